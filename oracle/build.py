@@ -1,0 +1,31 @@
+"""Build the CPU oracle into ``oracle/liboracle.so`` with gcc.
+
+Test infrastructure only (see ``oracle.c``). Plain C99, OpenMP, -O2 and no
+fast-math flags, so double-precision arithmetic follows IEEE 754 in program
+order.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(HERE, "oracle.c")
+LIBRARY = os.path.join(HERE, "liboracle.so")
+
+CFLAGS = ["-std=c99", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fPIC",
+          "-shared", "-fopenmp", "-Wall", "-Wextra"]
+
+
+def build(source: str = SOURCE, output: str = LIBRARY, extra: list[str] | None = None) -> str:
+    """Compile ``source`` into the shared library ``output`` and return its path."""
+    tmp = output + ".tmp%d" % os.getpid()
+    cmd = ["gcc", *CFLAGS, *(extra or []), source, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, output)
+    return output
+
+
+if __name__ == "__main__":
+    print(build(*sys.argv[1:2]))
