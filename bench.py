@@ -1,0 +1,257 @@
+"""Benchmark: one decode step of paged GQA decode attention on one MI355X.
+
+A step is one ``sl_decode_attn`` call over the whole synthetic batch (the
+partitioner, the split-KV kernel and the log-sum-exp merge), with every input
+already resident in HBM. Prints one JSON line:
+
+  value      algorithmic bytes per step / wall time per step (GB/s), where the
+             algorithmic bytes are the K/V page bytes of every live token
+             (2 * D * bytes-per-element per token and KV head; FP8 adds the two
+             4-byte scales per page and KV head), q and out (2 * Hq * D * 2 per
+             sequence) and one 4-byte block-table entry per page;
+  roofline   the split-KV kernel alone: the same algorithmic bytes over its
+             average duration from HIP events recorded around it on the launch
+             stream; HBM-bound, peak 8 TB/s; ``traffic`` comes from the
+             committed rocprofv3 counter summary for this workload when it was
+             taken on the current kernel source, else null;
+  cpu_baseline  the fp64 CPU oracle timed on the host cores on a bounded
+             sample of the same batch (the sequences and the byte count are
+             named in ``sample``); its outputs are also compared with the GPU's.
+
+Single GPU only: ``--gpus`` above 1 exits with an explanation.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+PEAK_HBM_GBS = 8000.0
+METRIC = "decode-attn achieved HBM GB/s (% of MI355X peak) + decode steps/s, long-tail batch"
+KERNEL_SOURCES = ["paper_2504_15930_amd/csrc/decode_split.hip", "paper_2504_15930_amd/csrc/sl_internal.h"]
+
+
+def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                      kv_bytes: int, page_size: int = 16) -> int:
+    L = np.maximum(seq_lens.astype(np.int64), 0)
+    pages = -(-L // page_size)
+    kv = int(L.sum()) * num_kv_heads * 2 * head_dim * kv_bytes
+    scales = int(pages.sum()) * num_kv_heads * 2 * 4 if kv_bytes == 1 else 0
+    qo = len(L) * 2 * num_q_heads * head_dim * 2
+    table = int(pages.sum()) * 4
+    return kv + scales + qo + table
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_counter_summary(workload: str) -> dict | None:
+    """key = value lines of profiles/decode_split_<workload>_counters.txt, if present."""
+    path = os.path.join(ROOT, "profiles", f"decode_split_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    out = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                out[k.strip()] = v.strip()
+    return out
+
+
+def traffic_bytes(workload: str) -> float | None:
+    c = read_counter_summary(workload)
+    if not c or c.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    try:
+        fetch = float(c["fetch_kib_per_dispatch"]) * float(c["fetch_scale"])
+        write = float(c["write_kib_per_dispatch"]) * float(c["write_scale"])
+    except (KeyError, ValueError):
+        return None
+    return (fetch + write) * 1024.0
+
+
+def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
+    """Time the oracle on a growing seeded sample of sequences until ~target_s of CPU work."""
+    import torch
+
+    import oracle
+
+    L = batch.seq_lens.cpu().numpy()
+    order = list(np.random.default_rng(123).permutation(len(L)))
+    Hq, D = batch.q.shape[1], batch.q.shape[2]
+    Hkv = batch.k_pages.shape[1]
+    kvb = 1 if batch.kv_dtype == "e4m3" else 2
+
+    def run(rows):
+        bt = batch.block_table[rows].cpu().numpy()
+        lens = L[rows]
+        nb = -(-np.maximum(lens, 0) // 16)
+        used = np.unique(np.concatenate([bt[i, :nb[i]] for i in range(len(rows))]))
+        remap = np.zeros(int(used.max()) + 1, dtype=np.int32)
+        remap[used] = np.arange(len(used), dtype=np.int32)
+        new_bt = np.zeros_like(bt)
+        for i in range(len(rows)):
+            new_bt[i, :nb[i]] = remap[bt[i, :nb[i]]]
+        idx = torch.as_tensor(used.astype(np.int64), device=batch.k_pages.device)
+
+        def bits(t):
+            t = t.cpu().contiguous()
+            return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+        args = dict(q=bits(batch.q[rows]), k_pages=bits(batch.k_pages.index_select(0, idx)),
+                    v_pages=bits(batch.v_pages.index_select(0, idx)))
+        kw = {}
+        if kvb == 1:
+            kw = dict(k_scales=batch.k_scales.index_select(0, idx).cpu().numpy(),
+                      v_scales=batch.v_scales.index_select(0, idx).cpu().numpy())
+        t0 = time.perf_counter()
+        ref = oracle.decode_attn(args["q"], args["k_pages"], args["v_pages"], new_bt, lens,
+                                 batch.scale, threads=threads, **kw)
+        return ref, time.perf_counter() - t0
+
+    n = 1
+    rows = order[:n]
+    ref, dt = run(rows)
+    while dt < target_s / 4 and n < len(L):
+        rate = max(dt, 1e-3) / max(1, int(L[rows].sum()))
+        want_tokens = target_s / rate
+        cum = np.cumsum(L[order])
+        n = int(min(len(L), max(n + 1, np.searchsorted(cum, want_tokens) + 1)))
+        rows = order[:n]
+        ref, dt = run(rows)
+    nbytes = algorithmic_bytes(L[rows], Hq, Hkv, D, kvb)
+    g = out_gpu[rows].float().cpu().double().numpy()
+    err = float(np.abs(g - ref).max())
+    rel = float((np.sqrt(((g - ref) ** 2).sum(-1)) / np.maximum(np.sqrt((ref ** 2).sum(-1)), 1e-30)).max())
+    return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", cores=oracle.max_threads(threads),
+                kind="oracle", seconds=round(dt, 3),
+                sample=f"{len(rows)} of {len(L)} sequences ({int(L[rows].sum())} tokens, "
+                       f"{nbytes / 1e6:.1f} MB algorithmic), seeded choice",
+                parity_vs_gpu=dict(max_abs_err=err, max_row_rel_l2=rel))
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen7b_longtail")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--workers", type=int, default=0, help="split-KV workers (0: library default)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline (0 disables it)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the decode-attention path here runs on a single "
+              "MI355X and has no multi-GPU mode; run it with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2504_15930_amd import inputs, sl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = inputs.WORKLOADS[args.workload]
+    print(f"[bench] generating {args.workload} (seed {args.seed})", file=sys.stderr, flush=True)
+    batch = inputs.make_batch(args.workload, seed=args.seed, device=dev)
+    torch.cuda.synchronize()
+    L = batch.seq_lens.cpu().numpy()
+    kvb = 1 if batch.kv_dtype == "e4m3" else 2
+    nbytes = algorithmic_bytes(L, w.num_q_heads, w.num_kv_heads, w.head_dim, kvb)
+    out = torch.empty_like(batch.q)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        sl.run_batch(batch, out=out, num_workers=args.workers)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for e in starts + stops:
+        e.record()                          # creates the underlying hipEvent
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    wall0 = time.perf_counter()
+    t_all0.record()
+    for i in range(args.steps):
+        sl.run_batch(batch, out=out, num_workers=args.workers,
+                     timing=(starts[i].cuda_event, stops[i].cuda_event))
+    t_all1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    step_ms = t_all0.elapsed_time(t_all1) / args.steps
+    wall_ms = wall * 1e3 / args.steps
+    kern_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
+    kern_avg = float(np.mean(kern_ms))
+    gbs = nbytes / (step_ms * 1e-3) / 1e9
+    achieved = nbytes / (kern_avg * 1e-3) / 1e9
+    workers = sl.num_workers(sl.make_desc(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, 16,
+                                          batch.block_table.shape[1], batch.k_pages.shape[0],
+                                          args.workers), fp8=kvb == 1)
+    result = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2),
+        "steps_per_s": round(1e3 / step_ms, 2),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 5),
+        "wall_ms_per_step": round(wall_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "e4m3 KV, bf16 q/out, fp32 accumulate" if kvb == 1 else "bf16 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "batch": w.batch, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim, "page_size": 16, "kv_dtype": batch.kv_dtype,
+            "total_tokens": int(L.sum()), "max_seq_len": int(L.max()),
+            "algorithmic_bytes": nbytes, "workers": workers, "seed": args.seed,
+        },
+        "roofline": {
+            "kernel": "split_kv_kernel",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic_bytes(args.workload),
+            "kernel_ms": round(kern_avg, 5),
+            "kernel_ms_p10_p90": [round(float(np.percentile(kern_ms, 10)), 5),
+                                  round(float(np.percentile(kern_ms, 90)), 5)],
+            "algorithmic_bytes_per_launch": nbytes,
+            "kernel_source_sha": kernel_source_hash(),
+        },
+    }
+    if args.cpu_seconds > 0:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(batch, out, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,154 @@
+/*
+ * libsl: batched GQA decode attention over a paged KV cache, for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * One call performs the attention part of one decode step of a batch of
+ * in-flight samples, each attending over its own growing context (StreamRL,
+ * Section 2.1: in the decoding phase every sample computes only its newest
+ * token and reuses the key-value cache of all earlier tokens; Section 2.4: the
+ * decode batch holds hundreds of samples whose output lengths are
+ * long-tailed; Section 6: continuous batching releases finished samples
+ * early, so lengths in one batch are ragged, and prefix sharing lets samples
+ * reference the same cache pages). The cache is paged as in PagedAttention
+ * (cited in Section 8): page `block_table[b][i]` of the pool holds tokens
+ * [i * page_size, (i + 1) * page_size) of sequence b.
+ *
+ * For every sequence b and query head h (G = num_q_heads / num_kv_heads,
+ * KV head g = h / G, L = seq_lens[b]):
+ *
+ *   out[b][h][:] = sum_t softmax_t(scale * q[b][h] . K_t) * V_t,  t < L
+ *
+ * and out[b][h][:] = 0 when L == 0. Arithmetic: bf16 inputs, fp32 scores and
+ * accumulators (softmax probabilities enter the value product rounded to
+ * bf16), bf16 output rounded to nearest even.
+ *
+ * Conventions shared by every entry point:
+ *  - All array pointers are device memory of the current HIP device, owned by
+ *    the caller; the library keeps no pointer after the call returns and
+ *    allocates nothing.
+ *  - Calls are asynchronous: work is enqueued on desc->stream and the call
+ *    returns; the caller synchronises. No host<->device copy and no host
+ *    synchronisation happen inside a call.
+ *  - Errors are reported by the returned sl_status; nothing throws across the
+ *    ABI. Argument checks happen before any work is enqueued, so an error
+ *    status means nothing was enqueued (SL_ERR_HIP excepted: a launch may
+ *    have failed part-way).
+ *  - Device-side data errors cannot be reported by status (the host never
+ *    reads seq_lens or block_table). They never cause an out-of-bounds
+ *    access: a sequence with seq_lens[b] < 0 or > max_blocks_per_seq *
+ *    page_size, or whose live block-table entries name a page outside
+ *    [0, num_pages), gets NaN in all its output rows.
+ *  - Calls sharing one workspace must not overlap in time (e.g. run them on
+ *    one stream).
+ */
+#ifndef SL_H
+#define SL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sl_status {
+    SL_OK = 0,
+    SL_ERR_NULL = -1,        /* a required pointer is NULL */
+    SL_ERR_SHAPE = -2,       /* a size is negative, zero where it must not be, or inconsistent */
+    SL_ERR_UNSUPPORTED = -3, /* valid but not implemented: head_dim, page_size, group size, batch */
+    SL_ERR_WORKSPACE = -4,   /* workspace NULL, too small or not 256-byte aligned */
+    SL_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed */
+    SL_ERR_ALIGNMENT = -6    /* q, out or a page pool not 16-byte aligned; block_table,
+                                seq_lens or a scale array not 4-byte aligned */
+} sl_status;
+
+/*
+ * Sizes of one decode step. Layouts (row-major, innermost last):
+ *   q, out          [batch][num_q_heads][head_dim]                 bf16
+ *   k_pages,v_pages [num_pages][num_kv_heads][page_size][head_dim] bf16 or e4m3
+ *   k_scales,...    [num_pages][num_kv_heads]                      fp32 (fp8 only)
+ *   block_table     [batch][max_blocks_per_seq]                    int32
+ *   seq_lens        [batch]                                        int32
+ * Supported: head_dim 64 or 128; page_size 16; 1 <= num_q_heads /
+ * num_kv_heads <= 16; batch <= 8192; batch * max_blocks_per_seq *
+ * num_kv_heads < 2^31.
+ */
+typedef struct sl_attn_desc {
+    int32_t batch;              /* sequences in the step; 0 makes every call a no-op */
+    int32_t num_q_heads;        /* Hq */
+    int32_t num_kv_heads;       /* Hkv; divides Hq; query head h reads KV head h / (Hq / Hkv) */
+    int32_t head_dim;           /* D */
+    int32_t page_size;          /* tokens per page */
+    int32_t max_blocks_per_seq; /* row length of block_table */
+    int32_t num_pages;          /* pages in each pool; valid page ids are [0, num_pages) */
+    int32_t num_workers;        /* 0: library default (one per resident wavefront of
+                                   the device); > 0: use exactly this many workers.
+                                   The result does not depend on it beyond fp32
+                                   rounding; tests vary it to exercise the merge. */
+    hipStream_t stream;         /* stream the work is enqueued on (0: null stream) */
+    void *workspace;            /* device scratch, >= sl_decode_attn_workspace_size bytes,
+                                   256-byte aligned; contents need no initialisation */
+    size_t workspace_bytes;
+    hipEvent_t timing_start;    /* optional (may be NULL): recorded on `stream` right */
+    hipEvent_t timing_stop;     /* before and after the split-KV kernel, for profiling */
+} sl_attn_desc;
+
+/*
+ * Bytes of workspace the calls need for `desc` (sizes and num_workers; no
+ * pointer is read). With num_workers == 0 this queries the current device.
+ * Errors: SL_ERR_NULL, SL_ERR_SHAPE, SL_ERR_UNSUPPORTED, SL_ERR_HIP.
+ */
+sl_status sl_decode_attn_workspace_size(const sl_attn_desc *desc, size_t *bytes);
+
+/*
+ * Number of workers (wavefronts of the split-KV kernel) a call with `desc`
+ * would use: desc->num_workers when positive, else the device default for the
+ * bf16 (kv_fp8 == 0) or FP8 (kv_fp8 != 0) kernel. Errors as
+ * sl_decode_attn_workspace_size.
+ */
+sl_status sl_decode_attn_num_workers(const sl_attn_desc *desc, int32_t kv_fp8,
+                                     int32_t *num_workers);
+
+/*
+ * Decode attention with a bf16 KV cache (formula above).
+ *   q            bf16 bits [batch][Hq][D]
+ *   k_pages      bf16 bits [num_pages][Hkv][page_size][D]
+ *   v_pages      bf16 bits, same shape
+ *   block_table  [batch][max_blocks_per_seq]; only the first
+ *                ceil(seq_lens[b] / page_size) entries of row b are read;
+ *                rows may name the same pages (prefix sharing)
+ *   seq_lens     [batch] cached tokens per sequence, the newest included
+ *   scale        multiplies q . k (usually 1 / sqrt(D))
+ *   out          bf16 bits [batch][Hq][D], written entirely
+ * Slots of a page past a sequence's end may hold anything (NaN included).
+ * Errors: SL_ERR_NULL, SL_ERR_SHAPE, SL_ERR_UNSUPPORTED, SL_ERR_WORKSPACE,
+ * SL_ERR_ALIGNMENT, SL_ERR_HIP.
+ */
+sl_status sl_decode_attn(const sl_attn_desc *desc, const uint16_t *q,
+                         const uint16_t *k_pages, const uint16_t *v_pages,
+                         const int32_t *block_table, const int32_t *seq_lens,
+                         float scale, uint16_t *out);
+
+/*
+ * Decode attention with an FP8 KV cache: pages hold OCP FP8 E4M3 codes
+ * (exponent bias 7, largest finite 448, 0x7F / 0xFF are NaN) and the cached
+ * value of element d of token t in (page, KV head g) is
+ * e4m3(code) * k_scales[page][g] for keys and * v_scales[page][g] for values.
+ * Everything else is as sl_decode_attn. Errors: as sl_decode_attn.
+ */
+sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q,
+                             const uint8_t *k_pages, const uint8_t *v_pages,
+                             const float *k_scales, const float *v_scales,
+                             const int32_t *block_table, const int32_t *seq_lens,
+                             float scale, uint16_t *out);
+
+/* Static English description of a status code (never NULL). */
+const char *sl_status_string(sl_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SL_H */

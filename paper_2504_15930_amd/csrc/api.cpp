@@ -1,0 +1,268 @@
+// Host side of libsl: argument checks, workspace layout, launch geometry and
+// the three launches of one decode-attention call (partition -> split-KV ->
+// merge), all enqueued on the caller's stream with no host synchronisation.
+#include <mutex>
+
+#include "../../include/sl.h"
+#include "sl_internal.h"
+
+namespace sl {
+
+static size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_workers,
+                        Workspace *ws)
+{
+    char *p = static_cast<char *>(base);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char *r = p ? p + off : nullptr;
+        off += align_up(bytes);
+        return r;
+    };
+    Workspace w;
+    w.cum_pages = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
+    w.worker_unit = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)num_workers));
+    w.part_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
+    w.part_acc = reinterpret_cast<float *>(
+        take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
+    if (ws)
+        *ws = w;
+    return off;
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int kMaxWorkers = 1 << 20;
+
+struct DeviceInfo {
+    std::once_flag once;
+    hipError_t err = hipSuccess;
+    int cus = 0;
+    int blocks[2][2] = {{0, 0}, {0, 0}};   // [head_dim == 128][fp8]
+};
+DeviceInfo g_devices[kMaxDevices];
+
+hipError_t device_info(DeviceInfo **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    DeviceInfo &d = g_devices[dev];
+    std::call_once(d.once, [&d, dev] {
+        d.err = hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev);
+        for (int hd = 0; hd < 2 && d.err == hipSuccess; ++hd)
+            for (int f = 0; f < 2 && d.err == hipSuccess; ++f)
+                d.err = split_blocks_per_cu(hd ? 128 : 64, f != 0, &d.blocks[hd][f]);
+    });
+    *out = &d;
+    return d.err;
+}
+
+sl_status check_desc(const sl_attn_desc *d)
+{
+    if (!d)
+        return SL_ERR_NULL;
+    if (d->batch < 0 || d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->head_dim <= 0 ||
+        d->page_size <= 0 || d->max_blocks_per_seq <= 0 || d->num_pages <= 0 ||
+        d->num_workers < 0)
+        return SL_ERR_SHAPE;
+    if (d->num_q_heads % d->num_kv_heads != 0)
+        return SL_ERR_SHAPE;
+    if (d->num_q_heads / d->num_kv_heads > kMaxGroup)
+        return SL_ERR_UNSUPPORTED;
+    if (d->head_dim != 64 && d->head_dim != 128)
+        return SL_ERR_UNSUPPORTED;
+    if (d->page_size != kPageSize)
+        return SL_ERR_UNSUPPORTED;
+    if (d->batch > kMaxBatch)
+        return SL_ERR_UNSUPPORTED;
+    if ((long long)d->batch * d->max_blocks_per_seq * d->num_kv_heads >= (1LL << 31) ||
+        (long long)d->max_blocks_per_seq * kPageSize >= (1LL << 31))
+        return SL_ERR_UNSUPPORTED;
+    if (d->num_workers > kMaxWorkers)
+        return SL_ERR_UNSUPPORTED;
+    return SL_OK;
+}
+
+sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
+{
+    if (d->num_workers > 0) {
+        *nw = d->num_workers;
+        return SL_OK;
+    }
+    DeviceInfo *info = nullptr;
+    if (device_info(&info) != hipSuccess)
+        return SL_ERR_HIP;
+    const int blocks = info->blocks[d->head_dim == 128][fp8 ? 1 : 0];
+    *nw = info->cus * (blocks > 0 ? blocks : 1) * kWavesPerBlock;
+    if (*nw > kMaxWorkers)
+        *nw = kMaxWorkers;
+    return SL_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, const void *v_pages,
+              const float *k_scales, const float *v_scales, const int32_t *block_table,
+              const int32_t *seq_lens, float scale, uint16_t *out, bool fp8)
+{
+    sl_status st = check_desc(d);
+    if (st != SL_OK)
+        return st;
+    if (d->batch == 0)
+        return SL_OK;
+    if (!q || !k_pages || !v_pages || !block_table || !seq_lens || !out)
+        return SL_ERR_NULL;
+    if (fp8 && (!k_scales || !v_scales))
+        return SL_ERR_NULL;
+    if (!aligned16(q) || !aligned16(out) || !aligned16(k_pages) || !aligned16(v_pages))
+        return SL_ERR_ALIGNMENT;
+    if (!aligned4(block_table) || !aligned4(seq_lens) ||
+        (fp8 && (!aligned4(k_scales) || !aligned4(v_scales))))
+        return SL_ERR_ALIGNMENT;
+    int nw = 0;
+    st = resolve_workers(d, fp8, &nw);
+    if (st != SL_OK)
+        return st;
+    const int G = d->num_q_heads / d->num_kv_heads;
+    Workspace ws;
+    const size_t need = workspace_layout(d->workspace, d->batch, G, d->head_dim, nw, &ws);
+    if (!d->workspace || d->workspace_bytes < need ||
+        (reinterpret_cast<uintptr_t>(d->workspace) & (kAlign - 1)) != 0)
+        return SL_ERR_WORKSPACE;
+
+    PartitionParams pp;
+    pp.seq_lens = seq_lens;
+    pp.cum_pages = ws.cum_pages;
+    pp.worker_unit = ws.worker_unit;
+    pp.batch = d->batch;
+    pp.num_kv_heads = d->num_kv_heads;
+    pp.max_blocks = d->max_blocks_per_seq;
+    pp.num_workers = nw;
+    if (launch_partition(pp, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+
+    SplitParams sp;
+    sp.q = q;
+    sp.k_pages = k_pages;
+    sp.v_pages = v_pages;
+    sp.k_scales = k_scales;
+    sp.v_scales = v_scales;
+    sp.block_table = block_table;
+    sp.seq_lens = seq_lens;
+    sp.out = out;
+    sp.cum_pages = ws.cum_pages;
+    sp.worker_unit = ws.worker_unit;
+    sp.part_ml = ws.part_ml;
+    sp.part_acc = ws.part_acc;
+    sp.batch = d->batch;
+    sp.num_q_heads = d->num_q_heads;
+    sp.num_kv_heads = d->num_kv_heads;
+    sp.group = G;
+    sp.max_blocks = d->max_blocks_per_seq;
+    sp.num_pages = d->num_pages;
+    sp.num_workers = nw;
+    sp.scale_log2 = scale * 1.4426950408889634f;
+    if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (launch_split(sp, d->head_dim, fp8, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+
+    MergeParams mp;
+    mp.seq_lens = seq_lens;
+    mp.cum_pages = ws.cum_pages;
+    mp.part_ml = ws.part_ml;
+    mp.part_acc = ws.part_acc;
+    mp.out = out;
+    mp.batch = d->batch;
+    mp.num_q_heads = d->num_q_heads;
+    mp.num_kv_heads = d->num_kv_heads;
+    mp.group = G;
+    mp.head_dim = d->head_dim;
+    mp.max_blocks = d->max_blocks_per_seq;
+    mp.num_workers = nw;
+    if (launch_merge(mp, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    return SL_OK;
+}
+
+}  // namespace
+}  // namespace sl
+
+extern "C" {
+
+sl_status sl_decode_attn_num_workers(const sl_attn_desc *desc, int32_t kv_fp8,
+                                     int32_t *num_workers)
+{
+    sl_status st = sl::check_desc(desc);
+    if (st != SL_OK)
+        return st;
+    if (!num_workers)
+        return SL_ERR_NULL;
+    int nw = 0;
+    st = sl::resolve_workers(desc, kv_fp8 != 0, &nw);
+    if (st == SL_OK)
+        *num_workers = nw;
+    return st;
+}
+
+sl_status sl_decode_attn_workspace_size(const sl_attn_desc *desc, size_t *bytes)
+{
+    sl_status st = sl::check_desc(desc);
+    if (st != SL_OK)
+        return st;
+    if (!bytes)
+        return SL_ERR_NULL;
+    // Size for the larger of the bf16 and fp8 worker counts, so one workspace serves both.
+    int nw_bf16 = 0, nw_fp8 = 0;
+    st = sl::resolve_workers(desc, false, &nw_bf16);
+    if (st == SL_OK)
+        st = sl::resolve_workers(desc, true, &nw_fp8);
+    if (st != SL_OK)
+        return st;
+    const int nw = nw_bf16 > nw_fp8 ? nw_bf16 : nw_fp8;
+    *bytes = sl::workspace_layout(nullptr, desc->batch, desc->num_q_heads / desc->num_kv_heads,
+                                  desc->head_dim, nw, nullptr);
+    return SL_OK;
+}
+
+sl_status sl_decode_attn(const sl_attn_desc *desc, const uint16_t *q, const uint16_t *k_pages,
+                         const uint16_t *v_pages, const int32_t *block_table,
+                         const int32_t *seq_lens, float scale, uint16_t *out)
+{
+    return sl::run(desc, q, k_pages, v_pages, nullptr, nullptr, block_table, seq_lens, scale, out,
+                   false);
+}
+
+sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q, const uint8_t *k_pages,
+                             const uint8_t *v_pages, const float *k_scales, const float *v_scales,
+                             const int32_t *block_table, const int32_t *seq_lens, float scale,
+                             uint16_t *out)
+{
+    return sl::run(desc, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale,
+                   out, true);
+}
+
+const char *sl_status_string(sl_status status)
+{
+    switch (status) {
+    case SL_OK: return "success";
+    case SL_ERR_NULL: return "a required pointer is NULL";
+    case SL_ERR_SHAPE: return "a size is negative, zero or inconsistent";
+    case SL_ERR_UNSUPPORTED: return "unsupported head_dim, page_size, group size or batch";
+    case SL_ERR_WORKSPACE: return "workspace missing, too small or not 256-byte aligned";
+    case SL_ERR_HIP: return "HIP runtime call or kernel launch failed";
+    case SL_ERR_ALIGNMENT: return "q, out or a page pool not 16-byte aligned, or an int/scale array not 4-byte aligned";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

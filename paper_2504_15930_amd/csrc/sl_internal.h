@@ -1,0 +1,86 @@
+// Internal interface between the host-side entry points (api.cpp) and the
+// gfx950 kernels (partition.hip, decode_split.hip, merge.hip).
+//
+// Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
+// n_b = ceil(L_b / 16) page-head tiles (16 tokens x head_dim of one KV head).
+// Units are laid out b-major, g-minor, and their tiles are numbered
+// consecutively, giving W = Hkv * sum_b n_b tiles in total. Worker w (one
+// wavefront) owns tiles [floor(w W / NW), floor((w + 1) W / NW)): every worker
+// reads the same number of tiles (+-1) whatever the length skew, so a few very
+// long sequences are spread over many workers instead of leaving most of the
+// chip idle (the on-chip analogue of StreamRL's skewness bubbles, Section 2.4
+// and Section 5.1). A unit that lies inside one worker's range is finished by
+// that worker; a unit cut by a range boundary leaves one partial softmax state
+// per worker that touched it, combined afterwards by the merge kernel.
+//
+// Partial slots: worker w writes the piece it started its range with to slot
+// 2w and, if its range ends inside a later unit, that piece to slot 2w + 1.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace sl {
+
+constexpr int kPageSize = 16;
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;          // split kernel: 4 independent workers per block
+constexpr int kMaxGroup = 16;              // query heads per KV head (one MFMA column block)
+constexpr int kMaxBatch = 8192;            // partitioner keeps one int per sequence in LDS
+constexpr int kPartitionThreads = 1024;
+constexpr int kMergeThreads = 256;
+constexpr size_t kAlign = 256;
+
+struct Workspace {
+    int32_t *cum_pages;    // [B + 1] exclusive prefix sum of pages per sequence
+    int32_t *worker_unit;  // [NW] unit holding each worker's first tile (-1: empty range)
+    float *part_ml;        // [2 NW][G][2]  (running max in log2 units, sum of weights)
+    float *part_acc;       // [2 NW][G][D]  un-normalised weighted value sums
+};
+
+struct PartitionParams {
+    const int32_t *seq_lens;
+    int32_t *cum_pages;
+    int32_t *worker_unit;
+    int32_t batch, num_kv_heads, max_blocks, num_workers;
+};
+
+struct SplitParams {
+    const uint16_t *q;
+    const void *k_pages;
+    const void *v_pages;
+    const float *k_scales;
+    const float *v_scales;
+    const int32_t *block_table;
+    const int32_t *seq_lens;
+    uint16_t *out;
+    const int32_t *cum_pages;
+    const int32_t *worker_unit;
+    float *part_ml;
+    float *part_acc;
+    int32_t batch, num_q_heads, num_kv_heads, group, max_blocks, num_pages, num_workers;
+    float scale_log2;      // scale * log2(e): scores are kept in base-2 units
+};
+
+struct MergeParams {
+    const int32_t *seq_lens;
+    const int32_t *cum_pages;
+    const float *part_ml;
+    const float *part_acc;
+    uint16_t *out;
+    int32_t batch, num_q_heads, num_kv_heads, group, head_dim, max_blocks, num_workers;
+};
+
+// Layout of the workspace for the given sizes; `base` may be null to size it.
+size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_workers,
+                        Workspace *ws);
+
+hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
+hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_merge(const MergeParams &p, hipStream_t stream);
+// Resident split-kernel workgroups per CU (occupancy query), for the default worker count.
+hipError_t split_blocks_per_cu(int head_dim, bool fp8, int *blocks);
+
+}  // namespace sl

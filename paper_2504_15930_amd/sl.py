@@ -1,0 +1,217 @@
+"""ctypes binding of ``libsl`` (``include/sl.h``): argument marshalling only.
+
+Every step of the decode-attention path runs in the HIP kernels of
+``libsl.so``; torch supplies device memory, the current stream and (for
+profiling) events. There is no fallback: without the built library or
+without a GPU tensor every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(HERE, "libsl.so")
+
+SL_OK = 0
+STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_UNSUPPORTED",
+                -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
+EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
+           "sl_decode_attn_fp8", "sl_status_string"]
+
+
+class SlError(RuntimeError):
+    """A libsl call returned an error status."""
+
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({status_string(status)})")
+
+
+class Desc(ctypes.Structure):
+    """Mirror of ``sl_attn_desc``."""
+
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("num_workers", ctypes.c_int32),
+        ("stream", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+        ("timing_start", ctypes.c_void_p),
+        ("timing_stop", ctypes.c_void_p),
+    ]
+
+
+_lib: ctypes.CDLL | None = None
+
+
+def load(path: str = LIBRARY) -> ctypes.CDLL:
+    """Load libsl (once). The HIP runtime torch already loaded is reused."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2504_15930_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    D = ctypes.POINTER(Desc)
+    lib.sl_decode_attn_workspace_size.argtypes = [D, ctypes.POINTER(ctypes.c_size_t)]
+    lib.sl_decode_attn_num_workers.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
+    lib.sl_decode_attn.argtypes = [D, P, P, P, P, P, ctypes.c_float, P]
+    lib.sl_decode_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_float, P]
+    lib.sl_status_string.argtypes = [ctypes.c_int]
+    lib.sl_status_string.restype = ctypes.c_char_p
+    for name in EXPORTS[:-1]:
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().sl_status_string(status).decode()
+
+
+def make_desc(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_blocks, num_pages,
+              num_workers=0, stream=None, workspace=None, workspace_bytes=0,
+              timing=None) -> Desc:
+    d = Desc()
+    d.batch, d.num_q_heads, d.num_kv_heads, d.head_dim = batch, num_q_heads, num_kv_heads, head_dim
+    d.page_size, d.max_blocks_per_seq, d.num_pages = page_size, max_blocks, num_pages
+    d.num_workers = num_workers
+    d.stream = stream
+    d.workspace = workspace
+    d.workspace_bytes = workspace_bytes
+    if timing is not None:
+        d.timing_start, d.timing_stop = timing
+    return d
+
+
+def _check(status: int, where: str):
+    if status != SL_OK:
+        raise SlError(status, where)
+
+
+def workspace_size(desc: Desc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().sl_decode_attn_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
+           "sl_decode_attn_workspace_size")
+    return n.value
+
+
+def num_workers(desc: Desc, fp8: bool = False) -> int:
+    n = ctypes.c_int32(0)
+    _check(load().sl_decode_attn_num_workers(ctypes.byref(desc), int(fp8), ctypes.byref(n)),
+           "sl_decode_attn_num_workers")
+    return n.value
+
+
+_workspaces: dict[int, torch.Tensor] = {}
+
+
+def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
+    """A cached per-device scratch buffer of at least ``nbytes`` (256-byte aligned by torch)."""
+    idx = device.index if device.index is not None else torch.cuda.current_device()
+    ws = _workspaces.get(idx)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _workspaces[idx] = ws
+    return ws
+
+
+def _need(t: torch.Tensor, name: str, dtype, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU (libsl has no CPU path)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _run(fp8, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, out,
+         num_workers_, workspace, timing):
+    kv_dtype = torch.uint8 if fp8 else torch.bfloat16
+    _need(q, "q", torch.bfloat16, 3)
+    _need(k_pages, "k_pages", kv_dtype, 4)
+    _need(v_pages, "v_pages", kv_dtype, 4)
+    _need(block_table, "block_table", torch.int32, 2)
+    _need(seq_lens, "seq_lens", torch.int32, 1)
+    if fp8:
+        _need(k_scales, "k_scales", torch.float32, 2)
+        _need(v_scales, "v_scales", torch.float32, 2)
+    B, Hq, D = q.shape
+    N, Hkv, P, D2 = k_pages.shape
+    if D2 != D or tuple(v_pages.shape) != tuple(k_pages.shape):
+        raise ValueError("q, k_pages and v_pages disagree on shape")
+    if block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_table / seq_lens rows must equal the batch")
+    if fp8 and (tuple(k_scales.shape) != (N, Hkv) or tuple(v_scales.shape) != (N, Hkv)):
+        raise ValueError("scales must have shape [num_pages, num_kv_heads]")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 3)
+        if out.shape != q.shape:
+            raise ValueError("out must have the shape of q")
+    with torch.cuda.device(q.device):
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+        desc = make_desc(B, Hq, Hkv, D, P, block_table.shape[1], N, num_workers_, stream)
+        if B == 0:
+            return out
+        need = workspace_size(desc)
+        ws = workspace if workspace is not None else _workspace(q.device, need)
+        desc.workspace = ws.data_ptr()
+        desc.workspace_bytes = ws.numel() * ws.element_size()
+        if timing is not None:
+            desc.timing_start, desc.timing_stop = timing
+        lib = load()
+        if fp8:
+            st = lib.sl_decode_attn_fp8(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(),
+                                        v_pages.data_ptr(), k_scales.data_ptr(), v_scales.data_ptr(),
+                                        block_table.data_ptr(), seq_lens.data_ptr(), float(scale),
+                                        out.data_ptr())
+            _check(st, "sl_decode_attn_fp8")
+        else:
+            st = lib.sl_decode_attn(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(),
+                                    v_pages.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
+                                    float(scale), out.data_ptr())
+            _check(st, "sl_decode_attn")
+    return out
+
+
+def decode_attn(q, k_pages, v_pages, block_table, seq_lens, scale, *, out=None, num_workers=0,
+                workspace=None, timing=None) -> torch.Tensor:
+    """``sl_decode_attn`` on torch tensors (bf16 KV cache); returns ``out`` [B, Hq, D] bf16.
+
+    ``timing`` optionally holds two raw hipEvent handles recorded around the
+    split-KV kernel. The call is asynchronous on the current stream.
+    """
+    return _run(False, q, k_pages, v_pages, None, None, block_table, seq_lens, scale, out,
+                num_workers, workspace, timing)
+
+
+def decode_attn_fp8(q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, *,
+                    out=None, num_workers=0, workspace=None, timing=None) -> torch.Tensor:
+    """``sl_decode_attn_fp8``: K/V pages are uint8 E4M3 codes with fp32 [N, Hkv] scales."""
+    return _run(True, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, out,
+                num_workers, workspace, timing)
+
+
+def run_batch(batch, **kw) -> torch.Tensor:
+    """Decode attention on an ``inputs.Batch`` (dispatches on its KV dtype)."""
+    if batch.kv_dtype == "e4m3":
+        return decode_attn_fp8(batch.q, batch.k_pages, batch.v_pages, batch.k_scales,
+                               batch.v_scales, batch.block_table, batch.seq_lens, batch.scale, **kw)
+    return decode_attn(batch.q, batch.k_pages, batch.v_pages, batch.block_table, batch.seq_lens,
+                       batch.scale, **kw)

@@ -1,0 +1,123 @@
+"""The C ABI on the host: the library loads, exports what include/sl.h declares,
+and rejects bad arguments before touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2504_15930_amd import sl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sl.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sl_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(sl.LIBRARY):
+        from paper_2504_15930_amd import build
+        build.build()
+    return sl.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(sl.EXPORTS), names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in sl.STATUS_NAMES:
+        assert len(sl.status_string(code)) > 5
+    assert sl.status_string(12345) == "unknown status"
+
+
+def _desc(**kw):
+    args = dict(batch=4, num_q_heads=8, num_kv_heads=2, head_dim=128, page_size=16, max_blocks=8,
+                num_pages=64, num_workers=32)
+    args.update(kw)
+    return sl.make_desc(**args)
+
+
+FAKE = 0x10000  # a 16-byte aligned address that is never dereferenced by these calls
+
+
+def _call(lib, d, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE):
+    return lib.sl_decode_attn(ctypes.byref(d) if d is not None else None, q, k, v, bt, lens,
+                              0.125, out)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_q_heads=7, num_kv_heads=2), -2),
+    (dict(batch=-1), -2),
+    (dict(num_pages=0), -2),
+    (dict(max_blocks=0), -2),
+    (dict(num_workers=-3), -2),
+    (dict(head_dim=96), -3),
+    (dict(page_size=32), -3),
+    (dict(num_q_heads=34, num_kv_heads=2), -3),
+    (dict(batch=9000), -3),
+    (dict(batch=8192, max_blocks=1 << 17, num_kv_heads=8, num_q_heads=8), -3),
+])
+def test_desc_validation(lib, kw, status):
+    d = _desc(**kw)
+    assert _call(lib, d) == status
+    n = ctypes.c_size_t(0)
+    assert lib.sl_decode_attn_workspace_size(ctypes.byref(d), ctypes.byref(n)) == status
+
+
+def test_null_and_alignment(lib):
+    assert _call(lib, None) == -1
+    d = _desc()
+    assert _call(lib, d, q=None) == -1
+    assert _call(lib, d, out=None) == -1
+    assert _call(lib, d, q=FAKE + 8) == -6
+    assert _call(lib, d, k=FAKE + 2) == -6
+    assert _call(lib, d, bt=FAKE + 2) == -6
+    assert _call(lib, d, bt=FAKE + 4) == -4          # 4-byte aligned is enough; no workspace
+    st = lib.sl_decode_attn_fp8(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                0.125, FAKE)
+    assert st == -1
+
+
+def test_batch_zero_is_a_noop(lib):
+    d = _desc(batch=0)
+    assert _call(lib, d, q=None, k=None, v=None, bt=None, lens=None, out=None) == 0
+
+
+def test_workspace_size_and_check(lib):
+    d = _desc(batch=4, num_workers=32, num_q_heads=8, num_kv_heads=2, head_dim=128)
+    n = sl.workspace_size(d)
+    align = lambda x: (x + 255) // 256 * 256
+    G = 4
+    assert n == align(4 * 5) + align(4 * 32) + align(4 * 2 * 32 * G * 2) + align(4 * 2 * 32 * G * 128)
+    assert sl.num_workers(d) == 32
+    d.workspace = None
+    assert _call(lib, d) == -4
+    d.workspace, d.workspace_bytes = 0x100000, n - 1
+    assert _call(lib, d) == -4
+    d.workspace, d.workspace_bytes = 0x100000 + 16, n + 64
+    assert _call(lib, d) == -4                        # not 256-byte aligned
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path")
+def test_default_workers_without_device(lib):
+    d = _desc(num_workers=0)
+    n = ctypes.c_size_t(0)
+    assert lib.sl_decode_attn_workspace_size(ctypes.byref(d), ctypes.byref(n)) == -5
+
+
+def test_binding_rejects_cpu_tensors(lib):
+    q = torch.zeros(2, 4, 64, dtype=torch.bfloat16)
+    k = torch.zeros(3, 2, 16, 64, dtype=torch.bfloat16)
+    bt = torch.zeros(2, 1, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU"):
+        sl.decode_attn(q, k, k, bt, torch.ones(2, dtype=torch.int32), 0.125)
