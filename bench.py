@@ -152,6 +152,9 @@ def main(argv=None) -> int:
     ap.add_argument("--workers", type=int, default=0, help="split-KV workers (0: library default)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline (0 disables it)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="instead of the benchmark, run `steps` plain device-to-device copies of "
+                         "BYTES bytes (the reference kernel for scaling HBM counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -165,6 +168,19 @@ def main(argv=None) -> int:
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        n = args.copy_calibration
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "steps": args.steps,
+                          "GBps_read_plus_write": round(2 * n / dt / 1e9, 1)}), flush=True)
+        return 0
     w = inputs.WORKLOADS[args.workload]
     print(f"[bench] generating {args.workload} (seed {args.seed})", file=sys.stderr, flush=True)
     batch = inputs.make_batch(args.workload, seed=args.seed, device=dev)

@@ -6,9 +6,11 @@ import torch
 
 import oracle
 
-# Tolerance for bf16 inputs with fp32 accumulation: every element within 1e-2
-# absolute of the fp64 oracle, and every (sequence, head) row within 2e-2 in
-# relative L2 norm.
+# Tolerance for bf16 inputs with fp32 accumulation and a bf16 output: absolute
+# 1e-2 and relative 2e-2, applied per element as |gpu - ref| <= ATOL + RTOL |ref|
+# (the bf16 output alone is rounded by up to 2^-9 |ref|, which exceeds 1e-2 once
+# |ref| > 5, so a bare 1e-2 bound cannot hold for large outputs), and per
+# (sequence, head) row as ||gpu - ref||_2 <= RTOL ||ref||_2.
 ATOL = 1e-2
 RTOL = 2e-2
 
@@ -19,8 +21,10 @@ def assert_parity(gpu: torch.Tensor, ref: np.ndarray, what: str = "", atol=ATOL,
     assert g.shape == ref.shape, f"{what}: shape {g.shape} vs {ref.shape}"
     assert np.isfinite(g).all(), f"{what}: non-finite GPU output at {np.argwhere(~np.isfinite(g))[:5]}"
     err = np.abs(g - ref)
-    worst = np.unravel_index(np.argmax(err), err.shape)
-    assert err.max() <= atol, f"{what}: max abs err {err.max():.3g} at {worst}"
+    excess = err - (atol + rtol * np.abs(ref))
+    worst = np.unravel_index(np.argmax(excess), err.shape)
+    assert excess.max() <= 0, (f"{what}: |err| {err[worst]:.3g} > {atol} + {rtol}|ref| "
+                               f"(ref {ref[worst]:.3g}) at {worst}; max abs err {err.max():.3g}")
     num = np.sqrt(((g - ref) ** 2).sum(axis=-1))
     den = np.sqrt((ref ** 2).sum(axis=-1))
     zero = den == 0
