@@ -73,6 +73,21 @@ def test_worker_count_independence(workers):
     assert_parity(out, ref, f"workers={workers}")
 
 
+def test_back_to_back_calls_share_the_workspace():
+    """Partial states of one call must never leak into the next (same shapes, new values)."""
+    _say("back to back calls")
+    a = inputs.make_paged_batch([900, 40, 1500, 333], 16, 2, 128, seed=21, device=DEV)
+    b = inputs.make_paged_batch([900, 40, 1500, 333], 16, 2, 128, seed=22, device=DEV)
+    ra, rb = oracle_full(a), oracle_full(b)
+    for workers in (0, 7, 64, 0):
+        for _ in range(3):
+            oa = sl.run_batch(a, num_workers=workers)
+            ob = sl.run_batch(b, num_workers=workers)
+        torch.cuda.synchronize()
+        assert_parity(oa, ra, f"first of pair, workers={workers}")
+        assert_parity(ob, rb, f"second of pair, workers={workers}")
+
+
 @pytest.mark.parametrize("kv", ["bf16", "e4m3"])
 def test_single_token_returns_value_row_exactly(kv):
     _say("single token", kv)
