@@ -10,8 +10,8 @@ namespace sl {
 
 static size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_workers,
-                        Workspace *ws)
+size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
+                        int head_dim, int num_workers, Workspace *ws)
 {
     char *p = static_cast<char *>(base);
     size_t off = 0;
@@ -22,7 +22,8 @@ size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_
     };
     Workspace w;
     w.cum_pages = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
-    w.worker_unit = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)num_workers));
+    w.tiles = reinterpret_cast<TileEntry *>(
+        take(sizeof(TileEntry) * (size_t)batch * max_blocks * num_kv_heads));
     w.part_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
     w.part_acc = reinterpret_cast<float *>(
         take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
@@ -34,7 +35,6 @@ size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_
 namespace {
 
 constexpr int kMaxDevices = 64;
-constexpr int kMaxWorkers = 1 << 16;
 
 struct DeviceInfo {
     std::once_flag once;
@@ -81,8 +81,13 @@ sl_status check_desc(const sl_attn_desc *d)
         return SL_ERR_UNSUPPORTED;
     if (d->batch > kMaxBatch)
         return SL_ERR_UNSUPPORTED;
-    if ((long long)d->batch * d->max_blocks_per_seq * d->num_kv_heads >= (1LL << 31) ||
-        (long long)d->max_blocks_per_seq * kPageSize >= (1LL << 31))
+    // Tile-list entries: at most 2^28 tiles (8-byte entries addressed with
+    // 32-bit byte offsets), page-head tile indices and query-row numbers that
+    // fit their fields.
+    if ((long long)d->batch * d->max_blocks_per_seq * d->num_kv_heads >= (1LL << 28) ||
+        (long long)d->max_blocks_per_seq * kPageSize >= (1LL << 31) ||
+        (long long)d->num_pages * d->num_kv_heads >= (1LL << 31) ||
+        (long long)d->batch * d->num_q_heads >= (1LL << (32 - kMetaRowShift)))
         return SL_ERR_UNSUPPORTED;
     if (d->num_workers > kMaxWorkers)
         return SL_ERR_UNSUPPORTED;
@@ -138,19 +143,22 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
         return st;
     const int G = d->num_q_heads / d->num_kv_heads;
     Workspace ws;
-    const size_t need = workspace_layout(d->workspace, d->batch, G, d->head_dim, nw, &ws);
+    const size_t need = workspace_layout(d->workspace, d->batch, d->max_blocks_per_seq,
+                                         d->num_kv_heads, G, d->head_dim, nw, &ws);
     if (!d->workspace || d->workspace_bytes < need ||
         (reinterpret_cast<uintptr_t>(d->workspace) & (kAlign - 1)) != 0)
         return SL_ERR_WORKSPACE;
 
     PartitionParams pp;
     pp.seq_lens = seq_lens;
+    pp.block_table = block_table;
     pp.cum_pages = ws.cum_pages;
-    pp.worker_unit = ws.worker_unit;
+    pp.tiles = ws.tiles;
     pp.batch = d->batch;
+    pp.num_q_heads = d->num_q_heads;
     pp.num_kv_heads = d->num_kv_heads;
     pp.max_blocks = d->max_blocks_per_seq;
-    pp.num_workers = nw;
+    pp.num_pages = d->num_pages;
     if (launch_partition(pp, d->stream) != hipSuccess)
         return SL_ERR_HIP;
 
@@ -160,19 +168,14 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     sp.v_pages = v_pages;
     sp.k_scales = k_scales;
     sp.v_scales = v_scales;
-    sp.block_table = block_table;
-    sp.seq_lens = seq_lens;
-    sp.out = out;
+    sp.tiles = ws.tiles;
     sp.cum_pages = ws.cum_pages;
-    sp.worker_unit = ws.worker_unit;
+    sp.out = out;
     sp.part_ml = ws.part_ml;
     sp.part_acc = ws.part_acc;
     sp.batch = d->batch;
-    sp.num_q_heads = d->num_q_heads;
     sp.num_kv_heads = d->num_kv_heads;
     sp.group = G;
-    sp.max_blocks = d->max_blocks_per_seq;
-    sp.num_pages = d->num_pages;
     sp.num_workers = nw;
     sp.scale_log2 = scale * 1.4426950408889634f;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
@@ -192,10 +195,8 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     mp.num_q_heads = d->num_q_heads;
     mp.num_kv_heads = d->num_kv_heads;
     mp.group = G;
-    mp.head_dim = d->head_dim;
-    mp.max_blocks = d->max_blocks_per_seq;
     mp.num_workers = nw;
-    if (launch_merge(mp, d->stream) != hipSuccess)
+    if (launch_merge(mp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     return SL_OK;
 }
@@ -235,7 +236,8 @@ sl_status sl_decode_attn_workspace_size(const sl_attn_desc *desc, size_t *bytes)
     if (st != SL_OK)
         return st;
     const int nw = nw_bf16 > nw_fp8 ? nw_bf16 : nw_fp8;
-    *bytes = sl::workspace_layout(nullptr, desc->batch, desc->num_q_heads / desc->num_kv_heads,
+    *bytes = sl::workspace_layout(nullptr, desc->batch, desc->max_blocks_per_seq,
+                                  desc->num_kv_heads, desc->num_q_heads / desc->num_kv_heads,
                                   desc->head_dim, nw, nullptr);
     return SL_OK;
 }

@@ -1,8 +1,10 @@
 // Split-KV decode attention kernel for gfx950.
 //
-// One wavefront is one worker; it walks its contiguous range of page-head
-// tiles (see sl_internal.h) and, for each (sequence, KV head) unit it touches,
-// keeps an online-softmax state for the G query heads that share the KV head.
+// One wavefront is one worker. It streams its contiguous range of page-head
+// tiles (see sl_internal.h) as a flat sequence, keeping an online-softmax
+// state for the G query heads of the unit (sequence, KV head) the current tile
+// belongs to, and finishing that unit whenever its last tile, or the end of
+// the range, is reached.
 //
 // Per 16-token tile, with lane = n + 16 * quad (n = lane & 15, quad = lane >> 4):
 //
@@ -18,11 +20,13 @@
 //           B = P^T exactly as the score MFMA left it (no data movement)
 //           -> lane (j, quad) accumulates O[j][d] for D/4 consecutive d
 //
-// K and V go straight from HBM into MFMA operand registers: there is no reuse
-// of a tile inside the workgroup, so an LDS round trip would only add
-// latency. Tiles are software-pipelined NBUF deep, and the block-table
-// entries of a piece are fetched 64 at a time, one per lane, a chunk ahead,
-// so a page id never waits on a dependent load.
+// K and V go straight from HBM into MFMA operand registers: a tile is used
+// by exactly one wave, so an LDS round trip would only add latency. They are
+// streamed with non-temporal loads. Tiles are software-pipelined kNbuf deep;
+// the tile-list entry (page and unit metadata) of a tile is fetched one
+// pipeline turn before the tile itself, and the query rows of a unit are
+// loaded together with the unit's first tile, so the stream never waits on a
+// dependent load, also across unit boundaries.
 //
 // FP8 pages hold OCP E4M3 codes; they are widened to bf16 exactly
 // (v_cvt_scalef32_pk_bf16_fp8 with unit scale), the per-(page, head) key
@@ -45,7 +49,8 @@ constexpr float kNegInf = -__builtin_inff();
 #ifndef SL_NBUF
 #define SL_NBUF 2
 #endif
-constexpr int kNbuf = SL_NBUF;   // tiles in the software pipeline
+constexpr int kNbuf = SL_NBUF;               // tiles in the software pipeline
+constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit buffer resource (CDNA3/4)
 
 __device__ __forceinline__ u32x4_t ld128(const uint8_t *p) { return *reinterpret_cast<const u32x4_t *>(p); }
 
@@ -82,6 +87,21 @@ __device__ __forceinline__ void e4m3x4_to_bf16(uint32_t codes, uint32_t &lo, uin
     hi = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes, 1.0f, true));
 }
 
+// Max / sum over the lanes n, n + 16, n + 32, n + 48 of a column.
+// (The gfx950 lane-swap builtins would avoid the LDS crossbar here, but this
+// compiler folds max(h[0], h[1]) of their two results to one of them, so the
+// plain shuffles are used.)
+__device__ __forceinline__ float quad_max(float x)
+{
+    x = fmaxf(x, __shfl_xor(x, 16, kWave));
+    return fmaxf(x, __shfl_xor(x, 32, kWave));
+}
+__device__ __forceinline__ float quad_sum(float x)
+{
+    x += __shfl_xor(x, 16, kWave);
+    return x + __shfl_xor(x, 32, kWave);
+}
+
 template <int D, bool FP8>
 struct Tile {
     // Per-lane dwords of K (score-MFMA A operands) and V (four rows).
@@ -89,14 +109,30 @@ struct Tile {
     static constexpr int VW = FP8 ? D / 16 : D / 8;
     uint32_t k[KW];
     uint32_t v[VW];
-    float scl;   // FP8: key scale in lanes 0-31, value scale in lanes 32-63
+    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only
+    float scl;           // FP8: key scale in lanes 0-31, value scale in lanes 32-63
+    uint32_t meta;       // TileEntry::meta (wave-uniform)
+    bool bad_page;       // the block table named a page outside the pool
 };
 
-// Issue the loads of one page-head tile. kt / vt point at the tile (uniform).
+// Query element index held by (quad, item) in k-step s; must match k_operand.
 template <int D, bool FP8>
-__device__ __forceinline__ void load_tile(Tile<D, FP8> &t, const uint8_t *kt, const uint8_t *vt,
-                                          const float *sp, int n, int quad)
+__device__ __forceinline__ int q_index(int s, int quad)
 {
+    return FP8 ? quad * (D / 4) + 8 * s : 32 * s + 8 * quad;
+}
+
+// Issue every load of one tile. All loads are unconditional.
+template <int D, bool FP8>
+__device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p, int32_t page,
+                                           uint32_t meta, bool with_q, int n, int quad, int lane)
+{
+    constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
+    t.meta = meta;
+    t.bad_page = page < 0;
+    const size_t tile = (size_t)(page < 0 ? 0 : page);
+    const uint8_t *kt = static_cast<const uint8_t *>(p.k_pages) + tile * kTileBytes;
+    const uint8_t *vt = static_cast<const uint8_t *>(p.v_pages) + tile * kTileBytes;
     if constexpr (!FP8) {
 #pragma unroll
         for (int s = 0; s < D / 32; ++s) {
@@ -138,7 +174,18 @@ __device__ __forceinline__ void load_tile(Tile<D, FP8> &t, const uint8_t *kt, co
                 t.v[r] = ld32_stream(src);
             }
         }
-        t.scl = *sp;
+        const float *sp = (lane & 32) ? p.v_scales : p.k_scales;
+        t.scl = sp[tile];
+    }
+    // The query rows of a unit travel with the unit's first tile (or the
+    // worker's first tile); lanes past the group read row G - 1 and are zeroed
+    // when the operand is formed.
+    if (with_q) {
+        const int G = p.group;
+        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s)
+            t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
     }
 }
 
@@ -158,30 +205,33 @@ __device__ __forceinline__ bf16x8_t k_operand(const Tile<D, FP8> &t, int s)
     return __builtin_bit_cast(bf16x8_t, w);
 }
 
-// Query element index held by (quad, item) in k-step s; must match k_operand.
-template <int D, bool FP8>
-__device__ __forceinline__ int q_index(int s, int quad)
-{
-    return FP8 ? quad * (D / 4) + 8 * s : 32 * s + 8 * quad;
-}
-
-template <int D, bool FP8>
+template <int D>
 struct Piece {
-    bf16x8_t q[D / 32];
     f32x4_t acc[D / 16];
     float m;   // running max of this lane's head, base-2 units
     float l;   // this lane's share of the sum of (bf16-rounded) weights
 };
 
+template <int D>
+__device__ __forceinline__ void reset(Piece<D> &st)
+{
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i)
+        st.acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    st.m = kNegInf;
+    st.l = 0.f;
+}
+
 // One tile of the online softmax. `valid` = live tokens in this page (1..16).
 template <int D, bool FP8>
-__device__ __forceinline__ void compute_tile(Piece<D, FP8> &st, const Tile<D, FP8> &t,
-                                             float score_mul, int valid, int quad)
+__device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t,
+                                             const bf16x8_t (&qop)[D / 32], float score_mul,
+                                             int valid, int quad)
 {
     f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
-        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(t, s), st.q[s], s4, 0, 0, 0);
+        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(t, s), qop[s], s4, 0, 0, 0);
 
     float vmul = 1.0f;
     if constexpr (FP8) {
@@ -199,28 +249,26 @@ __device__ __forceinline__ void compute_tile(Piece<D, FP8> &st, const Tile<D, FP
             if (4 * quad + r >= valid)
                 sc[r] = kNegInf;
     }
-    float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
     if (mx > st.m) {
-        const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on the first tile
+        const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a unit's first tile
         st.l *= alpha;
 #pragma unroll
         for (int i = 0; i < D / 16; ++i)
             st.acc[i] *= alpha;
         st.m = mx;
     }
-    float p[4];
+    float pr[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-        p[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
-    const uint32_t p01 = pack_bf16(p[0], p[1]);
-    const uint32_t p23 = pack_bf16(p[2], p[3]);
+        pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
+    const uint32_t p01 = pack_bf16(pr[0], pr[1]);
+    const uint32_t p23 = pack_bf16(pr[2], pr[3]);
     st.l += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
     i16x4_t pb;
     if constexpr (FP8) {
-        const uint32_t w01 = pack_bf16(p[0] * vmul, p[1] * vmul);
-        const uint32_t w23 = pack_bf16(p[2] * vmul, p[3] * vmul);
+        const uint32_t w01 = pack_bf16(pr[0] * vmul, pr[1] * vmul);
+        const uint32_t w23 = pack_bf16(pr[2] * vmul, pr[3] * vmul);
         pb = __builtin_bit_cast(i16x4_t, u32x2_t{w01, w23});
     } else {
         pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
@@ -262,101 +310,34 @@ __device__ __forceinline__ void compute_tile(Piece<D, FP8> &st, const Tile<D, FP
     }
 }
 
-template <int D, bool FP8>
-__device__ __forceinline__ void process_piece(const SplitParams &p, int w, int b, int g, int pg0,
-                                              int pg1, int nb, int slot_sel, bool full)
+// Finish the current unit: normalise and write its bf16 rows if the whole unit
+// was seen (`full`), else store the partial state in slot 2w + slot_sel.
+template <int D>
+__device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, uint32_t row0,
+                                            bool full, bool bad, int w, int slot_sel, int n, int quad)
 {
-    constexpr int ES = FP8 ? 1 : 2;                  // bytes per cached element
-    constexpr size_t kTileBytes = (size_t)kPageSize * D * ES;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int n = lane & 15;
-    const int quad = lane >> 4;
     const int G = p.group;
-    const int Hkv = p.num_kv_heads;
-    const int L = p.seq_lens[b];
-    bool bad = L < 0 || L > p.max_blocks * kPageSize;
-    const int last_valid = L - (nb - 1) * kPageSize;   // live tokens in page nb - 1
-
-    Piece<D, FP8> st;
-    const uint16_t *qrow = p.q + ((size_t)b * p.num_q_heads + (size_t)g * G + n) * D;
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
-        u32x4_t x = {0u, 0u, 0u, 0u};
-        if (n < G)
-            x = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
-        st.q[s] = __builtin_bit_cast(bf16x8_t, x);
-    }
-#pragma unroll
-    for (int i = 0; i < D / 16; ++i)
-        st.acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    st.m = kNegInf;
-    st.l = 0.f;
-
-    const uint8_t *kbase = static_cast<const uint8_t *>(p.k_pages) + (size_t)g * kTileBytes;
-    const uint8_t *vbase = static_cast<const uint8_t *>(p.v_pages) + (size_t)g * kTileBytes;
-    const size_t page_stride = (size_t)Hkv * kTileBytes;
-    const float *scale_src = (lane & 32) ? p.v_scales : p.k_scales;
-    const int32_t *bt_row = p.block_table + (size_t)b * p.max_blocks;
-
-    // Block-table entries for pages [c0, c0 + 64) (btc) and the next 64 (btn).
-    int c0 = pg0;
-    int btc = (c0 + lane < pg1) ? bt_row[c0 + lane] : 0;
-    int btn = (c0 + 64 + lane < pg1) ? bt_row[c0 + 64 + lane] : 0;
-
-    auto issue = [&](Tile<D, FP8> &t, int pg) {
-        if (pg - c0 >= 64) {
-            c0 += 64;
-            btc = btn;
-            btn = (c0 + 64 + lane < pg1) ? bt_row[c0 + 64 + lane] : 0;
-        }
-        int pid = __builtin_amdgcn_readlane(btc, pg - c0);
-        if ((unsigned)pid >= (unsigned)p.num_pages) {
-            bad = true;
-            pid = 0;
-        }
-        const size_t off = (size_t)pid * page_stride;
-        load_tile<D, FP8>(t, kbase + off, vbase + off,
-                          FP8 ? scale_src + (size_t)pid * Hkv + g : nullptr, n, quad);
-    };
-
-    Tile<D, FP8> buf[kNbuf];
-    const int np = pg1 - pg0;
-#pragma unroll
-    for (int k = 0; k < kNbuf - 1; ++k)
-        issue(buf[k], pg0 + min(k, np - 1));
-    for (int i0 = 0; i0 < np; i0 += kNbuf) {
-#pragma unroll
-        for (int k = 0; k < kNbuf; ++k) {
-            const int i = i0 + k;
-            issue(buf[(k + kNbuf - 1) % kNbuf], pg0 + min(i + kNbuf - 1, np - 1));
-            if (i < np) {
-                const int pg = pg0 + i;
-                compute_tile<D, FP8>(st, buf[k], p.scale_log2,
-                                     pg == nb - 1 ? last_valid : kPageSize, quad);
-            }
-        }
-    }
-
-    // Total weight of head n: sum the four quads' shares.
-    st.l += __shfl_xor(st.l, 16, kWave);
-    st.l += __shfl_xor(st.l, 32, kWave);
+    const float l = quad_sum(st.l);
+    const int d0 = quad * (D / 4);   // this lane holds O[row0 + n][d0 .. d0 + D/4)
     if (n >= G)
         return;
-    const int h = g * G + n;
-    const int d0 = quad * (D / 4);   // this lane holds O[h][d0 .. d0 + D/4)
     if (full) {
-        const float inv = bad ? __builtin_nanf("") : 1.0f / st.l;
-        uint32_t packed[D / 8];
+        const float inv = bad ? __builtin_nanf("") : 1.0f / l;
+        uint8_t *dst = reinterpret_cast<uint8_t *>(p.out + ((size_t)row0 + n) * D + d0);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int c = 0; c < D / 32; ++c) {
+            // output columns d0 + 8c .. 8c + 7 are acc[i][r] with r * D/16 + i = 8c + ...
+            uint32_t wv[4];
 #pragma unroll
-            for (int i = 0; i < D / 16; i += 2)
-                packed[(r * (D / 16) + i) / 2] = pack_bf16(st.acc[i][r] * inv, st.acc[i + 1][r] * inv);
-        uint8_t *dst = reinterpret_cast<uint8_t *>(p.out + ((size_t)b * p.num_q_heads + h) * D + d0);
-#pragma unroll
-        for (int c = 0; c < D / 32; ++c)
-            *reinterpret_cast<u32x4_t *>(dst + 16 * c) =
-                u32x4_t{packed[4 * c], packed[4 * c + 1], packed[4 * c + 2], packed[4 * c + 3]};
+            for (int e = 0; e < 4; ++e) {
+                const int k0 = 8 * c + 2 * e;   // flat index r * (D/16) + i
+                const int r0 = k0 / (D / 16), i0 = k0 % (D / 16);
+                const int k1 = k0 + 1;
+                const int r1 = k1 / (D / 16), i1 = k1 % (D / 16);
+                wv[e] = pack_bf16(st.acc[i0][r0] * inv, st.acc[i1][r1] * inv);
+            }
+            *reinterpret_cast<u32x4_t *>(dst + 16 * c) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
+        }
     } else {
         const size_t slot = 2 * (size_t)w + slot_sel;
         const float poison = bad ? __builtin_nanf("") : 0.0f;
@@ -367,8 +348,9 @@ __device__ __forceinline__ void process_piece(const SplitParams &p, int w, int b
             for (int i = 0; i < D / 16; i += 4)
                 *reinterpret_cast<f32x4_t *>(dst + r * (D / 16) + i) =
                     f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
-        if (quad == 0)
-            *reinterpret_cast<f32x2_t *>(p.part_ml + (slot * G + n) * 2) = f32x2_t{st.m, st.l};
+        if (quad == 0)   // a NaN maximum keeps the poison alive through the merge weights
+            *reinterpret_cast<f32x2_t *>(p.part_ml + (slot * G + n) * 2) =
+                f32x2_t{st.m + poison, l};
     }
 }
 
@@ -378,41 +360,93 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
     const int w = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (w >= p.num_workers)
         return;
-    const int Hkv = p.num_kv_heads;
-    const long long total = (long long)p.cum_pages[p.batch] * Hkv;
+    const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
     const long long s0 = (long long)w * total / p.num_workers;
     const long long s1 = (long long)(w + 1) * total / p.num_workers;
     if (s0 >= s1)
         return;
-    const int u = p.worker_unit[w];
-    if (u < 0)
-        return;
-    int b = u / Hkv;
-    int g = u - b * Hkv;
-    int cb = p.cum_pages[b];
-    int nb = p.cum_pages[b + 1] - cb;
-    int pg = (int)(s0 - ((long long)Hkv * cb + (long long)g * nb));
-    long long pos = s0;
+    const int ntiles = (int)(s1 - s0);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int n = lane & 15;
+    const int quad = lane >> 4;
+    const int G = p.group;
+
+    // This worker's tile-list entries, read through a bounds-checked buffer
+    // resource; an index past the range is clamped to the last tile.
+    const __amdgpu_buffer_rsrc_t ents = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<TileEntry *>(p.tiles + s0), 0, ntiles * (int)sizeof(TileEntry), kRawBufferWord3);
+    auto entry = [&](int i) -> u32x2_t {
+        const int j = i < ntiles ? i : ntiles - 1;
+        return __builtin_bit_cast(
+            u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
+    };
+    auto page_of = [](u32x2_t e) { return (int32_t)__builtin_amdgcn_readfirstlane(e[0]); };
+    auto meta_of = [](u32x2_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
+
+    // Ring of entries: slot k holds the entry of the tile issued at step k (mod
+    // kNbuf). The first entries and the ring are fetched together and waited
+    // for once here (the empty asm consumes them), so that inside the loop the
+    // counter wait for an entry only ever covers the loads of one pipeline turn
+    // and never drains the pipeline.
+    u32x2_t first[kNbuf - 1];
+#pragma unroll
+    for (int k = 0; k < kNbuf - 1; ++k)
+        first[k] = entry(k);
+    u32x2_t ring[kNbuf];
+#pragma unroll
+    for (int k = 0; k < kNbuf; ++k)
+        ring[k] = entry(kNbuf - 1 + k);
+#pragma unroll
+    for (int k = 0; k < kNbuf; ++k)
+        asm volatile("" ::"v"(ring[k]));
+    int32_t first_page[kNbuf - 1];
+    uint32_t first_meta[kNbuf - 1];
+#pragma unroll
+    for (int k = 0; k < kNbuf - 1; ++k) {
+        first_page[k] = page_of(first[k]);
+        first_meta[k] = meta_of(first[k]);
+    }
+
+    Tile<D, FP8> buf[kNbuf];
+#pragma unroll
+    for (int k = 0; k < kNbuf - 1; ++k)
+        issue_tile<D, FP8>(buf[k], p, first_page[k], first_meta[k],
+                           k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane);
+
+    Piece<D> st;
+    reset<D>(st);
+    bf16x8_t qop[D / 32];   // score-MFMA B operand of the current unit (zero rows j >= G)
+    bool started = false;   // the current unit's first tile is inside this range
+    bool bad = false;
     int slot_sel = 0;
-    while (pos < s1) {
-        const int take = (int)min((long long)(nb - pg), s1 - pos);
-        if (take <= 0 || pg < 0)
-            break;   // inconsistent partition: stop rather than loop
-        process_piece<D, FP8>(p, w, b, g, pg, pg + take, nb, slot_sel, pg == 0 && take == nb);
-        pos += take;
-        slot_sel = 1;
-        if (pos >= s1)
-            break;
-        pg = 0;
-        if (++g == Hkv) {
-            g = 0;
-            do {
-                if (b + 1 >= p.batch)
-                    return;   // inconsistent partition: no later unit exists
-                ++b;
-                cb = p.cum_pages[b];
-                nb = p.cum_pages[b + 1] - cb;
-            } while (nb == 0);
+    for (int i0 = 0; i0 < ntiles; i0 += kNbuf) {
+#pragma unroll
+        for (int k = 0; k < kNbuf; ++k) {
+            const int i = i0 + k;
+            const uint32_t next_meta = meta_of(ring[k]);
+            issue_tile<D, FP8>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
+                               (next_meta & kMetaFirst) != 0, n, quad, lane);
+            ring[k] = entry(i + 2 * kNbuf - 1);
+            if (i < ntiles) {
+                const Tile<D, FP8> &t = buf[k];
+                const uint32_t meta = t.meta;
+                if (i == 0 || (meta & kMetaFirst) != 0) {
+#pragma unroll
+                    for (int s = 0; s < D / 32; ++s)
+                        qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
+                }
+                started |= (meta & kMetaFirst) != 0;
+                bad |= t.bad_page || (meta & kMetaBadLen) != 0;
+                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, quad);
+                if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
+                    finish_unit<D>(p, st, meta >> kMetaRowShift, started && (meta & kMetaLast) != 0,
+                                   bad, w, slot_sel, n, quad);
+                    reset<D>(st);
+                    started = false;
+                    bad = false;
+                    slot_sel = 1;
+                }
+            }
         }
     }
 }

@@ -1,19 +1,24 @@
-// CU-level work partitioner: turns device-resident sequence lengths into the
-// tile ranges of the split-KV workers without any host synchronisation.
+// CU-level work partitioner: turns device-resident sequence lengths and block
+// tables into the flat tile list the split-KV workers stream, with no host
+// synchronisation.
 //
-// One workgroup of 1024 threads:
-//   1. pages per sequence, n_b = ceil(clamp(L_b, 0, max_blocks * 16) / 16),
-//      and their exclusive prefix sum (kept in LDS, copied to cum_pages);
-//   2. for each worker w, the unit (b, g) holding tile floor(w W / NW),
-//      found by binary search over the prefix sum.
-// Cost: O(B + NW log B) integer work, a few microseconds.
+// Every workgroup (1024 threads) first recomputes, in LDS, the pages per
+// sequence n_b = ceil(clamp(L_b, 0, max_blocks * 16) / 16) and their exclusive
+// prefix sum; workgroup 0 also stores that sum (cum_pages) for the other
+// kernels. Then the grid walks the live pages: page p of sequence b yields one
+// entry per KV head g at tile index Hkv * cum[b] + g * n_b + p, holding the
+// page-head tile index (page id * Hkv + g, or -1 for an id outside the pool)
+// and the unit's metadata (live tokens, first/last-tile flags, invalid-length
+// flag, first query row). Consecutive threads take consecutive pages of a
+// row, so block-table reads and entry writes are coalesced.
+// Cost: B prefix-sum work per workgroup plus 8 bytes written per tile.
 #include "sl_internal.h"
 
 namespace sl {
 
 __global__ __launch_bounds__(kPartitionThreads) void partition_kernel(PartitionParams p)
 {
-    __shared__ int32_t s_cum[kMaxBatch + 1];
+    extern __shared__ int32_t s_cum[];   // B + 1
     __shared__ int32_t s_part[kPartitionThreads / kWave];
 
     const int tid = threadIdx.x;
@@ -65,37 +70,57 @@ __global__ __launch_bounds__(kPartitionThreads) void partition_kernel(PartitionP
         s_cum[B] = s_part[kPartitionThreads / kWave - 1];
     __syncthreads();
 
-    for (int i = tid; i <= B; i += kPartitionThreads)
-        p.cum_pages[i] = s_cum[i];
+    if (blockIdx.x == 0)
+        for (int i = tid; i <= B; i += kPartitionThreads)
+            p.cum_pages[i] = s_cum[i];
 
     const int Hkv = p.num_kv_heads;
-    const long long total = (long long)s_cum[B] * Hkv;
-    const int NW = p.num_workers;
-    for (int w = tid; w < NW; w += kPartitionThreads) {
-        const long long s = (long long)w * total / NW;
-        const long long e = (long long)(w + 1) * total / NW;
-        if (s >= e) {
-            p.worker_unit[w] = -1;
-            continue;
-        }
-        // Largest b with Hkv * cum[b] <= s; then cum[b + 1] > s / Hkv, so n_b >= 1.
+    const int G = p.num_q_heads / Hkv;
+    const int total_pages = s_cum[B];
+    for (int x = blockIdx.x * kPartitionThreads + tid; x < total_pages;
+         x += gridDim.x * kPartitionThreads) {
+        // Largest b with cum[b] <= x; then cum[b + 1] > x, so n_b >= 1.
         int blo = 0, bhi = B;
         while (bhi - blo > 1) {
             const int mid = (blo + bhi) >> 1;
-            if ((long long)Hkv * s_cum[mid] <= s)
+            if (s_cum[mid] <= x)
                 blo = mid;
             else
                 bhi = mid;
         }
-        const long long nb = s_cum[blo + 1] - s_cum[blo];
-        const int g = (int)((s - (long long)Hkv * s_cum[blo]) / nb);
-        p.worker_unit[w] = blo * Hkv + g;
+        const int b = blo;
+        const int nb = s_cum[b + 1] - s_cum[b];
+        const int pg = x - s_cum[b];
+        const int L = p.seq_lens[b];
+        const int pid = p.block_table[(size_t)b * p.max_blocks + pg];
+        const bool page_ok = (unsigned)pid < (unsigned)p.num_pages;
+        const int live = min(kPageSize, L - pg * kPageSize);   // >= 1 for a valid length
+        uint32_t meta = (uint32_t)(max(live, 1) - 1);
+        if (pg == nb - 1)
+            meta |= kMetaLast;
+        if (pg == 0)
+            meta |= kMetaFirst;
+        if (L > max_len)
+            meta |= kMetaBadLen;
+        const long long base = (long long)Hkv * s_cum[b] + pg;
+        for (int g = 0; g < Hkv; ++g) {
+            TileEntry e;
+            e.page = page_ok ? pid * Hkv + g : -1;
+            e.meta = meta | ((uint32_t)(b * p.num_q_heads + g * G) << kMetaRowShift);
+            p.tiles[base + (long long)g * nb] = e;
+        }
     }
 }
 
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream)
 {
-    hipLaunchKernelGGL(partition_kernel, dim3(1), dim3(kPartitionThreads), 0, stream, p);
+    // Enough workgroups to give each thread about one page of the largest
+    // possible batch; the prefix sum is recomputed by every workgroup.
+    const long long max_pages = (long long)p.batch * p.max_blocks;
+    int grid = (int)((max_pages + kPartitionThreads - 1) / kPartitionThreads);
+    grid = grid < 1 ? 1 : (grid > 256 ? 256 : grid);
+    const size_t lds = sizeof(int32_t) * ((size_t)p.batch + 1);
+    hipLaunchKernelGGL(partition_kernel, dim3(grid), dim3(kPartitionThreads), lds, stream, p);
     return hipGetLastError();
 }
 

@@ -9,12 +9,17 @@
 // reads the same number of tiles (+-1) whatever the length skew, so a few very
 // long sequences are spread over many workers instead of leaving most of the
 // chip idle (the on-chip analogue of StreamRL's skewness bubbles, Section 2.4
-// and Section 5.1). A unit that lies inside one worker's range is finished by
-// that worker; a unit cut by a range boundary leaves one partial softmax state
-// per worker that touched it, combined afterwards by the merge kernel.
+// and Section 5.1).
 //
-// Partial slots: worker w writes the piece it started its range with to slot
-// 2w and, if its range ends inside a later unit, that piece to slot 2w + 1.
+// The partitioner writes one 8-byte entry per tile (TileEntry), so a worker
+// streams its range as one flat sequence of tiles: unit boundaries inside the
+// range cost no dependent load and do not drain the load pipeline.
+//
+// A unit that lies inside one worker's range is finished by that worker; a
+// unit cut by a range boundary leaves one partial softmax state per worker
+// that touched it, combined afterwards by the merge kernel. Worker w writes
+// the piece its range starts with to slot 2w and, if its range ends inside a
+// later unit, that trailing piece to slot 2w + 1.
 #pragma once
 
 #include <stddef.h>
@@ -28,23 +33,40 @@ constexpr int kPageSize = 16;
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;          // split kernel: 4 independent workers per block
 constexpr int kMaxGroup = 16;              // query heads per KV head (one MFMA column block)
-constexpr int kMaxBatch = 8192;            // partitioner keeps one int per sequence in LDS
+constexpr int kMaxBatch = 8192;            // the partitioner keeps one int per sequence in LDS
 constexpr int kPartitionThreads = 1024;
-constexpr int kMergeThreads = 256;
+constexpr int kMergeThreads = 256;         // one wave per unit, four units per block
+constexpr int kMaxWorkers = 1 << 16;       // keeps partial-state offsets below 2^31 bytes
 constexpr size_t kAlign = 256;
 
+// Tile entry. `page` = page_id * Hkv + g, the index of the tile in the
+// [num_pages][Hkv] grid of page-head tiles (-1: the block table named a page
+// outside the pool). `meta` packs, from bit 0:
+//   [3:0] live tokens in the tile minus one, [4] last tile of its unit,
+//   [5] first tile of its unit, [6] the sequence length is invalid,
+//   [31:8] first query row of the unit, b * Hq + g * G.
+struct TileEntry {
+    int32_t page;
+    uint32_t meta;
+};
+constexpr uint32_t kMetaLast = 1u << 4;
+constexpr uint32_t kMetaFirst = 1u << 5;
+constexpr uint32_t kMetaBadLen = 1u << 6;
+constexpr int kMetaRowShift = 8;
+
 struct Workspace {
-    int32_t *cum_pages;    // [B + 1] exclusive prefix sum of pages per sequence
-    int32_t *worker_unit;  // [NW] unit holding each worker's first tile (-1: empty range)
-    float *part_ml;        // [2 NW][G][2]  (running max in log2 units, sum of weights)
-    float *part_acc;       // [2 NW][G][D]  un-normalised weighted value sums
+    int32_t *cum_pages;   // [B + 1] exclusive prefix sum of pages per sequence
+    TileEntry *tiles;     // [B * max_blocks * Hkv] (the first W are used)
+    float *part_ml;       // [2 NW][G][2]  (running max in log2 units, sum of weights)
+    float *part_acc;      // [2 NW][G][D]  un-normalised weighted value sums
 };
 
 struct PartitionParams {
     const int32_t *seq_lens;
+    const int32_t *block_table;
     int32_t *cum_pages;
-    int32_t *worker_unit;
-    int32_t batch, num_kv_heads, max_blocks, num_workers;
+    TileEntry *tiles;
+    int32_t batch, num_q_heads, num_kv_heads, max_blocks, num_pages;
 };
 
 struct SplitParams {
@@ -53,14 +75,12 @@ struct SplitParams {
     const void *v_pages;
     const float *k_scales;
     const float *v_scales;
-    const int32_t *block_table;
-    const int32_t *seq_lens;
-    uint16_t *out;
+    const TileEntry *tiles;
     const int32_t *cum_pages;
-    const int32_t *worker_unit;
+    uint16_t *out;
     float *part_ml;
     float *part_acc;
-    int32_t batch, num_q_heads, num_kv_heads, group, max_blocks, num_pages, num_workers;
+    int32_t batch, num_kv_heads, group, num_workers;
     float scale_log2;      // scale * log2(e): scores are kept in base-2 units
 };
 
@@ -70,16 +90,16 @@ struct MergeParams {
     const float *part_ml;
     const float *part_acc;
     uint16_t *out;
-    int32_t batch, num_q_heads, num_kv_heads, group, head_dim, max_blocks, num_workers;
+    int32_t batch, num_q_heads, num_kv_heads, group, num_workers;
 };
 
 // Layout of the workspace for the given sizes; `base` may be null to size it.
-size_t workspace_layout(void *base, int batch, int group, int head_dim, int num_workers,
-                        Workspace *ws);
+size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
+                        int head_dim, int num_workers, Workspace *ws);
 
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
-hipError_t launch_merge(const MergeParams &p, hipStream_t stream);
+hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 // Resident split-kernel workgroups per CU (occupancy query), for the default worker count.
 hipError_t split_blocks_per_cu(int head_dim, bool fp8, int *blocks);
 

@@ -66,6 +66,8 @@ def _call(lib, d, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, lens=FAKE, out=FAKE):
     (dict(num_q_heads=34, num_kv_heads=2), -3),
     (dict(batch=9000), -3),
     (dict(batch=8192, max_blocks=1 << 17, num_kv_heads=8, num_q_heads=8), -3),
+    (dict(batch=4096, max_blocks=1 << 13, num_kv_heads=8, num_q_heads=8), -3),
+    (dict(num_pages=1 << 29, num_kv_heads=8, num_q_heads=8), -3),
     (dict(num_workers=65537), -3),
 ])
 def test_desc_validation(lib, kw, status):
@@ -99,7 +101,7 @@ def test_workspace_size_and_check(lib):
     n = sl.workspace_size(d)
     align = lambda x: (x + 255) // 256 * 256
     G = 4
-    assert n == (align(4 * 5) + align(4 * 32) + align(4 * 2 * 32 * G * 2)
+    assert n == (align(4 * 5) + align(8 * 4 * 8 * 2) + align(4 * 2 * 32 * G * 2)
                  + align(4 * 2 * 32 * G * 128))
     assert sl.num_workers(d) == 32
     d.workspace = None
