@@ -9,7 +9,8 @@
 // Per 16-token tile, with lane = n + 16 * quad (n = lane & 15, quad = lane >> 4):
 //
 //   scores  S^T[t][j] = sum_d K[t][d] Q[j][d]       v_mfma_f32_16x16x32_bf16
-//           A = K   (row t = n, 8 consecutive d per lane: one 16-byte load)
+//           A = K   (row t = n, 8 consecutive d per lane; the tile is read as
+//                    whole 1 KB runs and regrouped through LDS)
 //           B = Q^T (column j = n; query rows j >= G are zero padding)
 //           -> lane (j, quad) holds the scores of head j for tokens 4 quad + r
 //   softmax running max / sum per head j, kept in the lanes of column j: the
@@ -20,9 +21,12 @@
 //           B = P^T exactly as the score MFMA left it (no data movement)
 //           -> lane (j, quad) accumulates O[j][d] for D/4 consecutive d
 //
-// K and V go straight from HBM into MFMA operand registers: a tile is used
-// by exactly one wave, so an LDS round trip would only add latency. They are
-// streamed with non-temporal loads. Tiles are software-pipelined kNbuf deep;
+// V goes straight from HBM into MFMA operand registers: its loads already
+// cover whole 128-byte lines. The K operand layout would read only half a
+// line per instruction (each row spread over four lanes), which streams at
+// ~6.0 TB/s instead of ~6.85 TB/s on MI355X, so K is read in whole 1 KB runs
+// and regrouped through a small per-wave LDS buffer. Both are streamed with
+// non-temporal loads. Tiles are software-pipelined kNbuf deep;
 // the tile-list entry (page and unit metadata) of a tile is fetched one
 // pipeline turn before the tile itself, and the query rows of a unit are
 // loaded together with the unit's first tile, so the stream never waits on a
@@ -133,14 +137,17 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     const size_t tile = (size_t)(page < 0 ? 0 : page);
     const uint8_t *kt = static_cast<const uint8_t *>(p.k_pages) + tile * kTileBytes;
     const uint8_t *vt = static_cast<const uint8_t *>(p.v_pages) + tile * kTileBytes;
+    // K: whole 1 KB runs per instruction (lane l reads bytes 16 l of each
+    // run), so every instruction covers complete 128-byte lines; the rows are
+    // regrouped into the score-MFMA layout through LDS when the tile is used.
+#pragma unroll
+    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
+        const u32x4_t x = ld128_stream(kt + 1024 * i + 16 * lane);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            t.k[4 * i + c] = x[c];
+    }
     if constexpr (!FP8) {
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-            const u32x4_t x = ld128_stream(kt + (n * D + 32 * s + 8 * quad) * 2);
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                t.k[4 * s + c] = x[c];
-        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint8_t *src = vt + ((4 * quad + r) * D + n * (D / 16)) * 2;
@@ -156,13 +163,6 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
             }
         }
     } else {
-#pragma unroll
-        for (int h = 0; h < D / 64; ++h) {
-            const u32x4_t x = ld128_stream(kt + n * D + quad * (D / 4) + 16 * h);
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                t.k[4 * h + c] = x[c];
-        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint8_t *src = vt + (4 * quad + r) * D + n * (D / 16);
@@ -189,17 +189,46 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     }
 }
 
+// Regroup the K tile (loaded as whole 1 KB runs) into the score-MFMA layout
+// through this wave's LDS buffer: lane (t, quad) needs row t, and for bf16
+// the 16-byte chunks 4 s + quad (s = 0 .. D/32 - 1), for FP8 the D/64 chunks
+// starting at quad D/64. A chunk c of row r is stored at position
+// c ^ ((r / P) % C) of its row (P rows per 256 bytes, C chunks per row), which
+// makes the 16-lane groups of both the writes and the reads hit distinct banks.
+template <int D, bool FP8>
+__device__ __forceinline__ void regroup_k(const Tile<D, FP8> &t, uint8_t *lds, int lane, int n, int quad,
+                                          u32x4_t (&kc)[FP8 ? D / 64 : D / 32])
+{
+    constexpr int R = D * (FP8 ? 1 : 2);   // bytes per row
+    constexpr int C = R / 16;               // 16-byte chunks per row
+    constexpr int P = 256 / R;              // rows per 256 bytes
+#pragma unroll
+    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
+        const int off = 1024 * i + 16 * lane;
+        const int r = off / R, c = (off % R) / 16;
+        *reinterpret_cast<u32x4_t *>(lds + r * R + 16 * (c ^ ((r / P) % C))) =
+            u32x4_t{t.k[4 * i], t.k[4 * i + 1], t.k[4 * i + 2], t.k[4 * i + 3]};
+    }
+    const int key = (n / P) % C;
+#pragma unroll
+    for (int s = 0; s < (FP8 ? D / 64 : D / 32); ++s) {
+        const int c = FP8 ? quad * (D / 64) + s : 4 * s + quad;
+        kc[s] = *reinterpret_cast<const u32x4_t *>(lds + n * R + 16 * (c ^ key));
+    }
+}
+
 // Score-MFMA A operand for k-step s (8 bf16 values of row t = n).
 template <int D, bool FP8>
-__device__ __forceinline__ bf16x8_t k_operand(const Tile<D, FP8> &t, int s)
+__device__ __forceinline__ bf16x8_t k_operand(const u32x4_t (&kc)[FP8 ? D / 64 : D / 32], int s)
 {
     u32x4_t w;
     if constexpr (!FP8) {
-        w = u32x4_t{t.k[4 * s], t.k[4 * s + 1], t.k[4 * s + 2], t.k[4 * s + 3]};
+        w = kc[s];
     } else {
+        const uint32_t lo = kc[s / 2][2 * (s % 2)], hi = kc[s / 2][2 * (s % 2) + 1];
         uint32_t a, b, c, d;
-        e4m3x4_to_bf16(t.k[2 * s], a, b);
-        e4m3x4_to_bf16(t.k[2 * s + 1], c, d);
+        e4m3x4_to_bf16(lo, a, b);
+        e4m3x4_to_bf16(hi, c, d);
         w = u32x4_t{a, b, c, d};
     }
     return __builtin_bit_cast(bf16x8_t, w);
@@ -226,12 +255,14 @@ __device__ __forceinline__ void reset(Piece<D> &st)
 template <int D, bool FP8>
 __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t,
                                              const bf16x8_t (&qop)[D / 32], float score_mul,
-                                             int valid, int quad)
+                                             int valid, uint8_t *lds, int lane, int n, int quad)
 {
+    u32x4_t kc[FP8 ? D / 64 : D / 32];
+    regroup_k<D, FP8>(t, lds, lane, n, quad, kc);
     f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
-        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(t, s), qop[s], s4, 0, 0, 0);
+        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<D, FP8>(kc, s), qop[s], s4, 0, 0, 0);
 
     float vmul = 1.0f;
     if constexpr (FP8) {
@@ -370,6 +401,9 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
     const int n = lane & 15;
     const int quad = lane >> 4;
     const int G = p.group;
+    // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
+    __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
+    uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 
     // This worker's tile-list entries, read through a bounds-checked buffer
     // resource; an index past the range is clamped to the last tile.
@@ -437,7 +471,8 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
                 }
                 started |= (meta & kMetaFirst) != 0;
                 bad |= t.bad_page || (meta & kMetaBadLen) != 0;
-                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, quad);
+                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
+                                     quad);
                 if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
                     finish_unit<D>(p, st, meta >> kMetaRowShift, started && (meta & kMetaLast) != 0,
                                    bad, w, slot_sel, n, quad);
