@@ -195,23 +195,38 @@ def main(argv=None) -> int:
         sl.run_batch(batch, out=out, num_workers=args.workers)
     torch.cuda.synchronize()
 
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    for e in starts + stops:
-        e.record()                          # creates the underlying hipEvent
+    # Pass A (the headline): exactly `steps` whole calls, bracketed by events on
+    # the stream and nothing else inside the timed region.
     t_all0 = torch.cuda.Event(enable_timing=True)
     t_all1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     wall0 = time.perf_counter()
     t_all0.record()
     for i in range(args.steps):
-        sl.run_batch(batch, out=out, num_workers=args.workers,
-                     timing=(starts[i].cuda_event, stops[i].cuda_event))
+        sl.run_batch(batch, out=out, num_workers=args.workers)
     t_all1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+
+    # Pass B (the roofline): the same calls again, each with HIP events that the
+    # library records around the split-KV kernel on its launch stream. The
+    # extra event records lengthen the step slightly, so this pass only
+    # supplies the kernel's duration.
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for e in starts + stops:
+        e.record()                          # creates the underlying hipEvent
+    t_b0 = torch.cuda.Event(enable_timing=True)
+    t_b1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} split-KV kernels", file=sys.stderr, flush=True)
+    t_b0.record()
+    for i in range(args.steps):
+        sl.run_batch(batch, out=out, num_workers=args.workers,
+                     timing=(starts[i].cuda_event, stops[i].cuda_event))
+    t_b1.record()
+    torch.cuda.synchronize()
 
     step_ms = t_all0.elapsed_time(t_all1) / args.steps
     wall_ms = wall * 1e3 / args.steps
@@ -254,6 +269,7 @@ def main(argv=None) -> int:
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic_bytes(args.workload),
             "kernel_ms": round(kern_avg, 5),
+            "ms_per_step_with_kernel_events": round(t_b0.elapsed_time(t_b1) / args.steps, 5),
             "kernel_ms_p10_p90": [round(float(np.percentile(kern_ms, 10)), 5),
                                   round(float(np.percentile(kern_ms, 90)), 5)],
             "algorithmic_bytes_per_launch": nbytes,
