@@ -48,6 +48,10 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sl_oracle_decode_attn.restype = ctypes.c_int
     lib.sl_oracle_decode_attn.argtypes = [i, i, i, i, i, i, i, i, p, p, p, p, p, p, p,
                                           ctypes.c_float, p, i, p, i]
+    lib.sl_oracle_e4m3_encode.restype = ctypes.c_uint8
+    lib.sl_oracle_e4m3_encode.argtypes = [ctypes.c_float]
+    lib.sl_oracle_kv_append.restype = ctypes.c_int
+    lib.sl_oracle_kv_append.argtypes = [i, i, i, i, i, i, i, p, p, p, p, p, p, p, p]
     _LIBS[path] = lib
     return lib
 
@@ -125,3 +129,48 @@ def bf16_to_double(bits: int, lib: str | None = None) -> float:
 def max_threads(threads: int = 0, lib: str | None = None) -> int:
     """Threads the oracle's parallel loop uses for ``threads`` (0: default)."""
     return load(lib).sl_oracle_max_threads(threads)
+
+
+def e4m3_encode(values, lib=None) -> np.ndarray:
+    """OCP E4M3 codes (uint8) of float32 ``values``: nearest, ties to even, saturating, NaN -> 0x7F."""
+    lib = lib if isinstance(lib, ctypes.CDLL) else load(lib)
+    v = np.asarray(values, dtype=np.float32).ravel()
+    return np.array([lib.sl_oracle_e4m3_encode(ctypes.c_float(float(x))) for x in v],
+                    dtype=np.uint8).reshape(np.shape(values))
+
+
+def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, k_scales=None,
+              v_scales=None, lib=None):
+    """Append the step's new rows (see ``append.c``); returns updated copies.
+
+    ``k_new``/``v_new``: bf16 bits (uint16) [B, Hkv, D]. ``k_pages``/``v_pages``:
+    uint16 (bf16) or uint8 (E4M3 codes) [N, Hkv, P, D]; E4M3 needs fp32
+    ``k_scales``/``v_scales`` [N, Hkv]. Returns ``(k_pages, v_pages)`` or, for
+    E4M3, ``(k_pages, v_pages, k_scales, v_scales)``.
+    """
+    lib = lib if isinstance(lib, ctypes.CDLL) else load(lib)
+    kn = _arr(k_new, np.uint16)
+    vn = _arr(v_new, np.uint16)
+    bt = _arr(block_table, np.int32)
+    sl = _arr(seq_lens, np.int32)
+    kp = np.array(k_pages, copy=True, order="C")
+    vp = np.array(v_pages, copy=True, order="C")
+    fp8 = kp.dtype == np.uint8
+    if kp.dtype not in (np.uint8, np.uint16) or vp.dtype != kp.dtype:
+        raise TypeError("pages must be uint16 (bf16 bits) or uint8 (E4M3 codes)")
+    N, Hkv, P, D = kp.shape
+    B = kn.shape[0]
+    if kn.shape != (B, Hkv, D) or vn.shape != (B, Hkv, D) or bt.shape[0] != B or sl.shape != (B,):
+        raise ValueError("shape mismatch")
+    ks = vs = None
+    if fp8:
+        ks = np.array(k_scales, dtype=np.float32, copy=True, order="C")
+        vs = np.array(v_scales, dtype=np.float32, copy=True, order="C")
+        if ks.shape != (N, Hkv) or vs.shape != (N, Hkv):
+            raise ValueError("scales must be [N, Hkv]")
+    ptr = lambda a: None if a is None else a.ctypes.data
+    rc = lib.sl_oracle_kv_append(1 if fp8 else 0, B, Hkv, D, P, bt.shape[1], N, ptr(kn), ptr(vn),
+                                 ptr(bt), ptr(sl), ptr(kp), ptr(vp), ptr(ks), ptr(vs))
+    if rc != 0:
+        raise ValueError("oracle kv_append rejected its arguments")
+    return (kp, vp, ks, vs) if fp8 else (kp, vp)

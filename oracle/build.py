@@ -11,21 +11,28 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCE = os.path.join(HERE, "oracle.c")
+SOURCE = os.path.join(HERE, "oracle.c")           # decode attention
+SOURCES = [SOURCE, os.path.join(HERE, "append.c")]  # + KV append / E4M3 quantise-on-write
 LIBRARY = os.path.join(HERE, "liboracle.so")
 
 CFLAGS = ["-std=c99", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fPIC",
           "-shared", "-fopenmp", "-Wall", "-Wextra"]
 
 
-def build(source: str = SOURCE, output: str = LIBRARY, extra: list[str] | None = None) -> str:
-    """Compile ``source`` into the shared library ``output`` and return its path."""
+def build(sources: str | list[str] | None = None, output: str = LIBRARY,
+          extra: list[str] | None = None) -> str:
+    """Compile ``sources`` (default: every oracle source) into the shared library
+    ``output`` and return its path."""
+    if sources is None:
+        sources = SOURCES
+    elif isinstance(sources, str):
+        sources = [sources]
     tmp = output + ".tmp%d" % os.getpid()
-    cmd = ["gcc", *CFLAGS, *(extra or []), source, "-o", tmp, "-lm"]
+    cmd = ["gcc", *CFLAGS, *(extra or []), *sources, "-o", tmp, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, output)
     return output
 
 
 if __name__ == "__main__":
-    print(build(*sys.argv[1:2]))
+    print(build(sys.argv[1:] or None))

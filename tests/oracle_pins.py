@@ -384,9 +384,218 @@ def pin_golden_hand_worked(lib):
         _close(out, np.array(c["expected"]), c["rtol"], c["name"])
 
 
+# ------------------------------------------------------------- KV append pins
+#
+# The append step (oracle/append.c) is pinned the same way: torch's own
+# float8_e4m3fn conversion for the encoder, float64 SDPA over dense sequences
+# for where a bf16 row lands, torch-quantised whole pages for the FP8 scale
+# rule, an error bound for re-encoding, and a hand-derived fixture.
+
+E4M3_FN = torch.float8_e4m3fn
+
+
+def torch_e4m3(y: np.ndarray) -> np.ndarray:
+    """torch's float32 -> float8_e4m3fn codes after clamping to +-448 (saturation)."""
+    t = torch.from_numpy(np.asarray(y, dtype=np.float32)).clamp(-448.0, 448.0)
+    return t.to(E4M3_FN).view(torch.uint8).numpy().copy()
+
+
+def _e4m3_probe_values() -> np.ndarray:
+    finite = np.array([oracle.e4m3_to_double(c) for c in range(256)], dtype=np.float64)
+    finite = np.unique(finite[np.isfinite(finite)])                   # sorted, -448 .. 448
+    mids = (finite[:-1] + finite[1:]) / 2                             # exact ties
+    f32 = lambda x: np.asarray(x, dtype=np.float32)
+    around = np.concatenate([np.nextafter(f32(mids), f32(np.inf)), np.nextafter(f32(mids), f32(-np.inf))])
+    rng = np.random.default_rng(5)
+    rand = f32(np.exp(rng.uniform(np.log(2.0 ** -13), np.log(600.0), 3000)) * rng.choice([-1, 1], 3000))
+    big = f32([448.0, 449.0, 463.99, 464.0, 465.0, 480.0, 1e6, 3e38, np.inf, -np.inf, -470.0])
+    small = f32([0.0, -0.0, 2.0 ** -9, 2.0 ** -10, 3 * 2.0 ** -11, 2.0 ** -12, 1e-30, -1e-30, 2.0 ** -6, 0.015624])
+    return np.concatenate([f32(finite), f32(mids), around, rand, big, small])
+
+
+def pin_e4m3_encode_torch(lib):
+    """The encoder equals torch's float8_e4m3fn conversion (after +-448 clamping) on every
+    code, every tie, both neighbours of every tie, subnormals, saturation and random values."""
+    y = _e4m3_probe_values()
+    got = oracle.e4m3_encode(y, lib=oracle.load(lib))
+    want = torch_e4m3(y)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, f"encode differs from torch at {y[bad[:5]]}: {got[bad[:5]]} vs {want[bad[:5]]}"
+    assert oracle.e4m3_encode(np.array([np.nan], np.float32), lib=oracle.load(lib))[0] == 0x7F
+
+
+def _append_case(rng, lengths, Hkv, D, P, fp8):
+    """Pages holding each sequence's first L-1 tokens, plus the step's new rows."""
+    lengths = np.asarray(lengths, dtype=np.int32)
+    B = len(lengths)
+    Lmax = max(int(lengths.max(initial=0)), 1)
+    k_log = bf16_bits(rng.standard_normal((B, Lmax, Hkv, D)) * rng.uniform(0.2, 5.0, (B, Lmax, 1, 1)))
+    v_log = bf16_bits(rng.standard_normal((B, Lmax, Hkv, D)) * rng.uniform(0.2, 5.0, (B, Lmax, 1, 1)))
+    before = np.maximum(lengths - 1, 0)
+    sub = np.random.default_rng(int(rng.integers(1 << 31)))
+    k_pages, bt = scatter_pages(k_log, lengths, P, sub, BF16_NAN)
+    v_pages, _ = scatter_pages(v_log, lengths, P, sub, BF16_NAN, table=bt, num_pages=k_pages.shape[0])
+    # the new token's slot is not written yet: poison it
+    for b in range(B):
+        if lengths[b] >= 1:
+            t = lengths[b] - 1
+            k_pages[bt[b, t // P], :, t % P, :] = BF16_NAN
+            v_pages[bt[b, t // P], :, t % P, :] = BF16_NAN
+    idx = np.maximum(lengths - 1, 0)
+    k_new = k_log[np.arange(B), idx]                                  # [B, Hkv, D]
+    v_new = v_log[np.arange(B), idx]
+    return dict(lengths=lengths, before=before, bt=bt, k_pages=k_pages, v_pages=v_pages,
+                k_new=k_new, v_new=v_new, k_log=k_log, v_log=v_log)
+
+
+def pin_append_bf16_dense(lib):
+    """After appending the new rows, attention over the pages equals float64 SDPA over the
+    dense sequences that end with those rows, and no other slot changed."""
+    rng = np.random.default_rng(21)
+    P, Hkv, D, G = 16, 2, 64, 3
+    lengths = [1, 15, 16, 17, 33, 0, 48, 2]
+    c = _append_case(rng, lengths, Hkv, D, P, fp8=False)
+    kp, vp = oracle.kv_append(c["k_new"], c["v_new"], c["bt"], c["lengths"], c["k_pages"],
+                              c["v_pages"], lib=oracle.load(lib))
+    changed = np.any(kp != c["k_pages"], axis=-1) | np.any(vp != c["v_pages"], axis=-1)
+    expect = np.zeros_like(changed)
+    for b, L in enumerate(lengths):
+        if L >= 1:
+            expect[c["bt"][b, (L - 1) // P], :, (L - 1) % P] = True
+    assert np.array_equal(changed, expect), "append wrote outside the new tokens' slots"
+    q = bf16_bits(rng.standard_normal((len(lengths), Hkv * G, D)))
+    scale = float(np.float32(1 / 8))
+    out = oracle.decode_attn(q, kp, vp, c["bt"], c["lengths"], scale, lib=lib)
+    ref = sdpa_reference(bits_f64(q), bits_f64(c["k_log"]), bits_f64(c["v_log"]), lengths, scale)
+    _close(out, ref, 1e-12, "append then attend vs dense sdpa")
+
+
+def _fp8_pages_from(c, P):
+    """E4M3 pages holding the first L-1 tokens quantised per (page, head) by torch."""
+    kp = c["k_pages"]
+    N, Hkv, _, D = kp.shape
+    out = []
+    for pages in (c["k_pages"], c["v_pages"]):
+        vals = bits_f64(pages).to(torch.float32)
+        live = torch.zeros((N, 1, P, 1), dtype=torch.bool)
+        for b, L in enumerate(c["lengths"]):
+            for t in range(max(int(L) - 1, 0)):
+                live[c["bt"][b, t // P], 0, t % P, 0] = True
+        amax = torch.where(live, vals.abs(), torch.zeros(())).amax(dim=(2, 3))
+        sc = torch.where(amax > 0, amax / 448.0, torch.ones(()))
+        codes = (vals / sc[:, :, None, None]).clamp(-448, 448).to(E4M3_FN).view(torch.uint8)
+        codes = torch.where(live, codes, torch.full((), 0x7F, dtype=torch.uint8))
+        out += [codes.numpy().copy(), sc.numpy().copy()]
+    return out
+
+
+def pin_append_fp8_fresh_page(lib):
+    """A row that opens a page gets scale amax/448 and torch's codes of row/scale; K and V
+    keep separate scales; nothing else changes."""
+    rng = np.random.default_rng(22)
+    P, Hkv, D = 16, 3, 64
+    lengths = [1, 17, 33, 49, 1]
+    c = _append_case(rng, lengths, Hkv, D, P, fp8=True)
+    kc, ks, vc, vs = _fp8_pages_from(c, P)
+    kp, vp, ks2, vs2 = oracle.kv_append(c["k_new"], c["v_new"], c["bt"], c["lengths"], kc, vc,
+                                        k_scales=ks, v_scales=vs, lib=oracle.load(lib))
+    for new, pages, scales, pages0, scales0, what in ((c["k_new"], kp, ks2, kc, ks, "K"),
+                                                     (c["v_new"], vp, vs2, vc, vs, "V")):
+        x = bits_f64(new).to(torch.float32)                           # [B, Hkv, D]
+        amax = x.abs().amax(-1)
+        sc = torch.where(amax > 0, amax / 448.0, torch.ones(())).numpy()
+        want = torch_e4m3((x / torch.from_numpy(sc)[..., None]).numpy())
+        mask = np.ones(pages.shape[:3], dtype=bool)
+        for b, L in enumerate(lengths):
+            pg = c["bt"][b, (L - 1) // P]
+            assert np.array_equal(scales[pg], sc[b]), f"{what} scale of a fresh page"
+            assert np.array_equal(pages[pg, :, 0, :], want[b]), f"{what} codes of a fresh page"
+            mask[pg, :, 0] = False
+        assert np.array_equal(pages[mask], pages0[mask]), f"{what}: other slots changed"
+
+
+def pin_append_fp8_largest_first(lib):
+    """Filling a page one row at a time, largest row first, never re-encodes: the result equals
+    torch quantising the whole page with scale = page amax / 448."""
+    rng = np.random.default_rng(23)
+    P, Hkv, D = 16, 2, 32
+    for trial in range(3):
+        x = rng.standard_normal((P, Hkv, D)) * np.exp(-np.arange(P) * 0.15)[:, None, None]
+        x[0] *= 3.0
+        xb = bf16_bits(x)
+        codes = np.full((1, Hkv, P, D), 0x7F, np.uint8)
+        sc = np.ones((1, Hkv), np.float32)
+        kc, vc, ks, vs = codes, codes.copy(), sc, sc.copy()
+        bt = np.zeros((1, 1), np.int32)
+        for t in range(P):
+            kc, vc, ks, vs = oracle.kv_append(xb[t][None], xb[t][None], bt, np.array([t + 1], np.int32),
+                                              kc, vc, k_scales=ks, v_scales=vs, lib=oracle.load(lib))
+        vals = bits_f64(xb).to(torch.float32).permute(1, 0, 2)        # [Hkv, P, D]
+        amax = vals.abs().amax(dim=(1, 2))
+        want_sc = torch.where(amax > 0, amax / 448.0, torch.ones(()))
+        want = torch_e4m3((vals / want_sc[:, None, None]).numpy())
+        assert np.array_equal(ks[0], want_sc.numpy()), f"trial {trial}: page scale"
+        assert np.array_equal(kc[0], want), f"trial {trial}: page codes"
+        assert np.array_equal(vc, kc) and np.array_equal(vs, ks)
+
+
+def pin_append_fp8_growing_rows(lib):
+    """Rows of growing magnitude force a re-encode on every append: the final scale is the last
+    row's amax/448 and every dequantised value stays within the rounding error of the encodes
+    it went through (one half step of the 3-bit mantissa per encode, or half the smallest
+    subnormal step at the final scale)."""
+    rng = np.random.default_rng(24)
+    P, D = 16, 64
+    mags = 0.01 * 1.7 ** np.arange(P)
+    x = rng.standard_normal((P, 1, D)) * mags[:, None, None]
+    for t in range(P):
+        x[t, 0, t % D] = 3.0 * mags[t] * (1 if t % 2 else -1)          # a clear maximum per row
+    xb = bf16_bits(x)
+    kc = np.full((1, 1, P, D), 0x7F, np.uint8)
+    ks = np.ones((1, 1), np.float32)
+    bt = np.zeros((1, 1), np.int32)
+    for t in range(P):
+        kc, _, ks, _ = oracle.kv_append(xb[t][None], xb[t][None], bt, np.array([t + 1], np.int32), kc,
+                                        kc.copy(), k_scales=ks, v_scales=ks.copy(), lib=oracle.load(lib))
+        s_t = np.float32(np.abs(bits_f64(xb[t]).numpy()).max()) / np.float32(448)
+        assert ks[0, 0] == s_t, f"scale after row {t}: {ks[0, 0]} vs {s_t}"
+    vals = bits_f64(xb).numpy()[:, 0, :]
+    deq = np.array([[oracle.e4m3_to_double(c) for c in row] for row in kc[0, 0]]) * float(ks[0, 0])
+    encodes = (P - np.arange(P))[:, None]                              # row t: 1 + (P-1-t) re-encodes
+    bound = encodes * (2.0 ** -4 * np.abs(vals) * 1.001 + 2.0 ** -10 * float(ks[0, 0])) + 1e-30
+    err = np.abs(deq - vals)
+    assert np.all(err <= bound), f"re-encode error {np.max(err / bound):.3f} x bound"
+
+
+def pin_golden_append(lib):
+    """Hand-derived quantise-on-write steps in tests/golden/append_worked.json."""
+    with open(os.path.join(GOLDEN, "append_worked.json")) as f:
+        g = json.load(f)
+    P, D = g["page_size"], g["head_dim"]
+    kc = np.full((1, 1, P, D), 0x7F, np.uint8)
+    vc = kc.copy()
+    ks = np.ones((1, 1), np.float32)
+    vs = ks.copy()
+    bt = np.zeros((1, 1), np.int32)
+    num = lambda v: np.array([float(x) for x in v], dtype=np.float32)
+    for st in g["steps"]:
+        kn = bf16_bits(num(st["k_new"]))[None, None]
+        vn = bf16_bits(num(st["v_new"]))[None, None]
+        assert np.array_equal(bits_f64(kn).numpy(), num(st["k_new"]).astype(np.float64)[None, None],
+                              equal_nan=True), "fixture rows must be exact in bf16"
+        kc, vc, ks, vs = oracle.kv_append(kn, vn, bt, np.array([st["seq_len"]], np.int32), kc, vc,
+                                          k_scales=ks, v_scales=vs, lib=oracle.load(lib))
+        n = st["seq_len"]
+        assert np.array_equal(kc[0, 0, :n], np.array(st["k_codes"], np.uint8)), f"K codes at {n}"
+        assert np.array_equal(vc[0, 0, :n], np.array(st["v_codes"], np.uint8)), f"V codes at {n}"
+        assert ks[0, 0] == np.float32(st["k_scale"]) and vs[0, 0] == np.float32(st["v_scale"]), f"scales at {n}"
+
+
 ALL_PINS = [
     pin_sdpa_random, pin_sdpa_large_scores, pin_prefix_sharing, pin_single_token,
     pin_identical_keys, pin_constant_values, pin_dominant_token, pin_page_permutation,
     pin_head_permutation, pin_zero_length, pin_rows_subset, pin_e4m3_table, pin_sdpa_fp8,
     pin_golden_hand_worked,
+    pin_e4m3_encode_torch, pin_append_bf16_dense, pin_append_fp8_fresh_page,
+    pin_append_fp8_largest_first, pin_append_fp8_growing_rows, pin_golden_append,
 ]

@@ -1,10 +1,11 @@
 """Planted mistakes in the oracle must trip at least one pin.
 
-Each case copies ``oracle/oracle.c``, plants one plausible mistake (a dropped
-term, a wrong index, a transposed layout, a wrong constant), builds the copy on
-the CPU and runs every pin of ``oracle_pins`` against it in a child process, so
-that a mutant which crashes also counts as caught. The real oracle is never
-modified.
+Each case copies one oracle source (``oracle/oracle.c`` for decode attention,
+``oracle/append.c`` for the KV append), plants one plausible mistake (a dropped
+term, a wrong index, a transposed layout, a wrong constant), builds the copy
+with the other sources on the CPU and runs every pin of ``oracle_pins`` against
+it in a child process, so that a mutant which crashes also counts as caught.
+The real oracle is never modified.
 """
 import os
 import subprocess
@@ -18,7 +19,7 @@ from oracle import build as oracle_build
 TESTS = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(TESTS)
 
-# (name, original text, replacement, which occurrence (0-based))
+# (name, original text, replacement, which occurrence (0-based)[, source file])
 MUTANTS = [
     ("head_map_modulo", "int g = h / G;", "int g = h % Hkv;", 0),
     ("block_table_transposed", "block_table[(size_t)b * max_blocks + t / P]",
@@ -44,6 +45,24 @@ MUTANTS = [
      "kv_value(kv_kind, k_pages, v_scales,", 0),
     ("scale_ignores_head", "scales[(size_t)page * Hkv + g]", "scales[(size_t)page * Hkv]", 0),
     ("bf16_shift", "uint32_t u = (uint32_t)bits << 16;", "uint32_t u = (uint32_t)bits << 15;", 0),
+    # KV append / E4M3 quantise-on-write
+    ("append_after_new_token", "const int t = L - 1;", "const int t = L;", 0, "append.c"),
+    ("append_head_stride", "const size_t tile = ((size_t)page * Hkv + g) * P * D;",
+     "const size_t tile = ((size_t)page * Hkv) * P * D;", 0, "append.c"),
+    ("append_scale_never_grows", "if (a <= reach) {", "if (1) {", 0, "append.c"),
+    ("append_no_reencode", "for (int j = 0; j < slot; ++j)", "for (int j = 0; j < 0; ++j)", 0, "append.c"),
+    ("append_reencode_keeps_old_scale", "*c = sl_oracle_e4m3_encode(v / s);",
+     "*c = sl_oracle_e4m3_encode(v / s_old);", 0, "append.c"),
+    ("append_fresh_page_keeps_scale", "if (slot == 0) {", "if (0) {", 0, "append.c"),
+    ("append_amax_signed", "const float v = fabsf(bf16_to_float(x[d]));", "const float v = bf16_to_float(x[d]);",
+     0, "append.c"),
+    ("append_kv_scales_swapped", "&k_scales[(size_t)page * Hkv + g]);", "&v_scales[(size_t)page * Hkv + g]);",
+     0, "append.c"),
+    ("encode_truncates", "double k = nearbyint((m - 1.0) * 8.0);", "double k = floor((m - 1.0) * 8.0);", 0,
+     "append.c"),
+    ("encode_no_saturation", "if (a >= 448.0)", "if (a >= 1e300)", 0, "append.c"),
+    ("encode_subnormal_step", "nearbyint(a / ldexp(1.0, -9))", "nearbyint(a / ldexp(1.0, -10))", 0, "append.c"),
+    ("encode_nan_as_zero", "return 0x7F;", "return 0x00;", 0, "append.c"),
 ]
 
 CHILD = r"""
@@ -69,13 +88,20 @@ def _mutate(src: str, old: str, new: str, occurrence: int) -> str:
     return src[:start] + new + src[start + len(old):]
 
 
-def _run_mutant(tmpdir, name, old, new, occ):
-    with open(oracle_build.SOURCE) as f:
-        src = f.read()
-    path = os.path.join(tmpdir, f"{name}.c")
-    with open(path, "w") as f:
-        f.write(_mutate(src, old, new, occ))
-    lib = oracle_build.build(path, os.path.join(tmpdir, f"lib{name}.so"), extra=["-w"])
+def _run_mutant(tmpdir, name, old, new, occ, fname="oracle.c"):
+    sources = []
+    for src_path in oracle_build.SOURCES:
+        if os.path.basename(src_path) == fname:
+            with open(src_path) as f:
+                src = f.read()
+            path = os.path.join(tmpdir, f"{name}_{fname}")
+            with open(path, "w") as f:
+                f.write(_mutate(src, old, new, occ))
+            sources.append(path)
+        else:
+            sources.append(src_path)
+    assert len(sources) == len(oracle_build.SOURCES) and any(tmpdir in s for s in sources), fname
+    lib = oracle_build.build(sources, os.path.join(tmpdir, f"lib{name}.so"), extra=["-w"])
     env = dict(os.environ, OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-c", CHILD.format(root=ROOT, tests=TESTS, lib=lib)],
                        capture_output=True, text=True, timeout=300, env=env)
