@@ -145,6 +145,63 @@ sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q,
                              const int32_t *block_table, const int32_t *seq_lens,
                              float scale, uint16_t *out);
 
+/*
+ * KV append: stores one decode step's new key and value rows in the paged
+ * cache, the step that precedes attention in every decode step (StreamRL,
+ * Section 2.1: each decoding step computes the newest token and keeps its
+ * per-token state in the key-value cache that later steps reuse).
+ *
+ * seq_lens already counts the new token (the same array the step's attention
+ * call takes): for every sequence b with L = seq_lens[b] >= 1 the row of the
+ * token t = L - 1 goes to page block_table[b][t / page_size], slot
+ * t % page_size, for every KV head g. L == 0 appends nothing.
+ *   k_new, v_new  bf16 bits [batch][Hkv][D], read only
+ *   block_table   [batch][max_blocks_per_seq]; only entry (L - 1) / page_size
+ *                 of row b is read
+ *   seq_lens      [batch]
+ *   k_pages, v_pages  the cache, written only in the new tokens' slots
+ * The page receiving a sequence's new token must not be the receiving page of
+ * another sequence in the same call (copy a shared last page first);
+ * otherwise the result for those sequences is unspecified (no fault).
+ * A sequence with seq_lens[b] < 0 or > max_blocks_per_seq * page_size, or
+ * whose receiving page id lies outside [0, num_pages), is left untouched.
+ * Uses desc fields batch, num_kv_heads, head_dim, page_size,
+ * max_blocks_per_seq, num_pages, stream, timing_start/timing_stop (optional
+ * events recorded around the kernel); num_q_heads must be valid as for
+ * attention; the workspace is not used.
+ * Errors: SL_ERR_NULL, SL_ERR_SHAPE, SL_ERR_UNSUPPORTED, SL_ERR_ALIGNMENT
+ * (k_new, v_new, block_table, seq_lens need 4-byte, pages 16-byte alignment),
+ * SL_ERR_HIP.
+ */
+sl_status sl_kv_append(const sl_attn_desc *desc, const uint16_t *k_new, const uint16_t *v_new,
+                       const int32_t *block_table, const int32_t *seq_lens,
+                       uint16_t *k_pages, uint16_t *v_pages);
+
+/*
+ * KV append into an FP8 (E4M3) cache with one fp32 scale per (page, KV head)
+ * for keys and another for values, quantising on write. The scale of a
+ * page-head tile only grows; with a = max_d |x_d| of the new row (NaN
+ * elements ignored):
+ *   slot 0 (the row opens the page):  scale = a / 448, or 1 if a == 0
+ *   a <= scale * 448:                 scale unchanged
+ *   a >  scale * 448:                 scale' = a / 448, and every earlier slot
+ *                                     j of the tile is re-encoded as
+ *                                     enc(e4m3(code) * scale / scale')
+ * and the new row is stored as enc(x_d / scale). enc rounds to nearest with
+ * ties to even, saturates to +-448 and maps NaN to 0x7F. All of this is
+ * binary32 arithmetic in the order written, so codes and scales are exact and
+ * reproducible. Keys and values are handled separately. The paper does not
+ * describe FP8 storage; this rule keeps every live slot of a tile encoded
+ * with the tile's current scale, which is what sl_decode_attn_fp8 reads.
+ *   k_pages, v_pages    E4M3 codes [num_pages][Hkv][page_size][D]
+ *   k_scales, v_scales  fp32 [num_pages][Hkv], read and written
+ * Everything else is as sl_kv_append (scales need 4-byte alignment).
+ */
+sl_status sl_kv_append_fp8(const sl_attn_desc *desc, const uint16_t *k_new, const uint16_t *v_new,
+                           const int32_t *block_table, const int32_t *seq_lens,
+                           uint8_t *k_pages, uint8_t *v_pages, float *k_scales,
+                           float *v_scales);
+
 /* Static English description of a status code (never NULL). */
 const char *sl_status_string(sl_status status);
 

@@ -201,10 +201,66 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     return SL_OK;
 }
 
+sl_status run_append(const sl_attn_desc *d, const uint16_t *k_new, const uint16_t *v_new,
+                     const int32_t *block_table, const int32_t *seq_lens, void *k_pages, void *v_pages,
+                     float *k_scales, float *v_scales, bool fp8)
+{
+    sl_status st = check_desc(d);
+    if (st != SL_OK)
+        return st;
+    if (d->batch == 0)
+        return SL_OK;
+    if (!k_new || !v_new || !block_table || !seq_lens || !k_pages || !v_pages)
+        return SL_ERR_NULL;
+    if (fp8 && (!k_scales || !v_scales))
+        return SL_ERR_NULL;
+    if (!aligned4(k_new) || !aligned4(v_new) || !aligned4(block_table) || !aligned4(seq_lens) ||
+        !aligned16(k_pages) || !aligned16(v_pages) ||
+        (fp8 && (!aligned4(k_scales) || !aligned4(v_scales))))
+        return SL_ERR_ALIGNMENT;
+    AppendParams ap;
+    ap.k_new = k_new;
+    ap.v_new = v_new;
+    ap.block_table = block_table;
+    ap.seq_lens = seq_lens;
+    ap.k_pages = k_pages;
+    ap.v_pages = v_pages;
+    ap.k_scales = k_scales;
+    ap.v_scales = v_scales;
+    ap.batch = d->batch;
+    ap.num_kv_heads = d->num_kv_heads;
+    ap.max_blocks = d->max_blocks_per_seq;
+    ap.num_pages = d->num_pages;
+    if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (launch_append(ap, d->head_dim, fp8, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    return SL_OK;
+}
+
 }  // namespace
 }  // namespace sl
 
 extern "C" {
+
+sl_status sl_kv_append(const sl_attn_desc *desc, const uint16_t *k_new, const uint16_t *v_new,
+                       const int32_t *block_table, const int32_t *seq_lens, uint16_t *k_pages,
+                       uint16_t *v_pages)
+{
+    return sl::run_append(desc, k_new, v_new, block_table, seq_lens, k_pages, v_pages, nullptr, nullptr,
+                          false);
+}
+
+sl_status sl_kv_append_fp8(const sl_attn_desc *desc, const uint16_t *k_new, const uint16_t *v_new,
+                           const int32_t *block_table, const int32_t *seq_lens, uint8_t *k_pages,
+                           uint8_t *v_pages, float *k_scales, float *v_scales)
+{
+    return sl::run_append(desc, k_new, v_new, block_table, seq_lens, k_pages, v_pages, k_scales, v_scales,
+                          true);
+}
+
 
 sl_status sl_decode_attn_num_workers(const sl_attn_desc *desc, int32_t kv_fp8,
                                      int32_t *num_workers)

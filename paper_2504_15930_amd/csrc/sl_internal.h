@@ -1,5 +1,5 @@
 // Internal interface between the host-side entry points (api.cpp) and the
-// gfx950 kernels (partition.hip, decode_split.hip, merge.hip).
+// gfx950 kernels (partition.hip, decode_split.hip, merge.hip, append.hip).
 //
 // Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
 // n_b = ceil(L_b / 16) page-head tiles (16 tokens x head_dim of one KV head).
@@ -93,6 +93,18 @@ struct MergeParams {
     int32_t batch, num_q_heads, num_kv_heads, group, num_workers;
 };
 
+struct AppendParams {
+    const uint16_t *k_new;      // [B][Hkv][D] bf16 rows of the step's new token
+    const uint16_t *v_new;
+    const int32_t *block_table;
+    const int32_t *seq_lens;    // already counting the new token
+    void *k_pages;              // bf16 or E4M3 pool [num_pages][Hkv][16][D]
+    void *v_pages;
+    float *k_scales;            // E4M3 only: [num_pages][Hkv]
+    float *v_scales;
+    int32_t batch, num_kv_heads, max_blocks, num_pages;
+};
+
 // Layout of the workspace for the given sizes; `base` may be null to size it.
 size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
                         int head_dim, int num_workers, Workspace *ws);
@@ -100,6 +112,7 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
+hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Resident split-kernel workgroups per CU (occupancy query), for the default worker count.
 hipError_t split_blocks_per_cu(int head_dim, bool fp8, int *blocks);
 

@@ -1,6 +1,6 @@
 """ctypes binding of ``libsl`` (``include/sl.h``): argument marshalling only.
 
-Every step of the decode-attention path runs in the HIP kernels of
+Every step of the decode path (KV append and attention) runs in the HIP kernels of
 ``libsl.so``; torch supplies device memory, the current stream and (for
 profiling) events. There is no fallback: without the built library or
 without a GPU tensor every entry point raises.
@@ -19,7 +19,7 @@ SL_OK = 0
 STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_UNSUPPORTED",
                 -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
-           "sl_decode_attn_fp8", "sl_status_string"]
+           "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_status_string"]
 
 
 class SlError(RuntimeError):
@@ -67,6 +67,8 @@ def load(path: str = LIBRARY) -> ctypes.CDLL:
     lib.sl_decode_attn_num_workers.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
     lib.sl_decode_attn.argtypes = [D, P, P, P, P, P, ctypes.c_float, P]
     lib.sl_decode_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_float, P]
+    lib.sl_kv_append.argtypes = [D, P, P, P, P, P, P]
+    lib.sl_kv_append_fp8.argtypes = [D, P, P, P, P, P, P, P, P]
     lib.sl_status_string.argtypes = [ctypes.c_int]
     lib.sl_status_string.restype = ctypes.c_char_p
     for name in EXPORTS[:-1]:
@@ -215,3 +217,49 @@ def run_batch(batch, **kw) -> torch.Tensor:
                                batch.v_scales, batch.block_table, batch.seq_lens, batch.scale, **kw)
     return decode_attn(batch.q, batch.k_pages, batch.v_pages, batch.block_table, batch.seq_lens,
                        batch.scale, **kw)
+
+
+def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, k_scales=None,
+              v_scales=None, num_q_heads=None, timing=None):
+    """``sl_kv_append`` / ``sl_kv_append_fp8`` on torch tensors, in place.
+
+    ``k_new``/``v_new``: bf16 [B, Hkv, D] rows of the step's new token;
+    ``seq_lens`` already counts it. A uint8 page pool selects the E4M3 path,
+    which needs fp32 ``k_scales``/``v_scales`` [N, Hkv] (updated in place).
+    Asynchronous on the current stream.
+    """
+    fp8 = k_pages.dtype == torch.uint8
+    kv_dtype = torch.uint8 if fp8 else torch.bfloat16
+    _need(k_new, "k_new", torch.bfloat16, 3)
+    _need(v_new, "v_new", torch.bfloat16, 3)
+    _need(k_pages, "k_pages", kv_dtype, 4)
+    _need(v_pages, "v_pages", kv_dtype, 4)
+    _need(block_table, "block_table", torch.int32, 2)
+    _need(seq_lens, "seq_lens", torch.int32, 1)
+    if fp8:
+        _need(k_scales, "k_scales", torch.float32, 2)
+        _need(v_scales, "v_scales", torch.float32, 2)
+    B, Hkv, D = k_new.shape
+    N, Hkv2, P, D2 = k_pages.shape
+    if (Hkv2, D2) != (Hkv, D) or tuple(v_new.shape) != (B, Hkv, D) or v_pages.shape != k_pages.shape:
+        raise ValueError("k_new / v_new / pages disagree on shape")
+    if block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_table / seq_lens rows must equal the batch")
+    if fp8 and (tuple(k_scales.shape) != (N, Hkv) or tuple(v_scales.shape) != (N, Hkv)):
+        raise ValueError("scales must have shape [num_pages, num_kv_heads]")
+    with torch.cuda.device(k_new.device):
+        stream = torch.cuda.current_stream(k_new.device).cuda_stream
+        desc = make_desc(B, num_q_heads or Hkv, Hkv, D, P, block_table.shape[1], N, 0, stream)
+        if timing is not None:
+            desc.timing_start, desc.timing_stop = timing
+        lib = load()
+        if fp8:
+            st = lib.sl_kv_append_fp8(ctypes.byref(desc), k_new.data_ptr(), v_new.data_ptr(),
+                                      block_table.data_ptr(), seq_lens.data_ptr(), k_pages.data_ptr(),
+                                      v_pages.data_ptr(), k_scales.data_ptr(), v_scales.data_ptr())
+            _check(st, "sl_kv_append_fp8")
+        else:
+            st = lib.sl_kv_append(ctypes.byref(desc), k_new.data_ptr(), v_new.data_ptr(),
+                                  block_table.data_ptr(), seq_lens.data_ptr(), k_pages.data_ptr(),
+                                  v_pages.data_ptr())
+            _check(st, "sl_kv_append")

@@ -125,3 +125,30 @@ def test_binding_rejects_cpu_tensors(lib):
     bt = torch.zeros(2, 1, dtype=torch.int32)
     with pytest.raises(ValueError, match="GPU"):
         sl.decode_attn(q, k, k, bt, torch.ones(2, dtype=torch.int32), 0.125)
+
+
+def _append(lib, d, fp8=False, kn=FAKE, vn=FAKE, bt=FAKE, lens=FAKE, kp=FAKE, vp=FAKE, ks=FAKE, vs=FAKE):
+    ref = ctypes.byref(d) if d is not None else None
+    if fp8:
+        return lib.sl_kv_append_fp8(ref, kn, vn, bt, lens, kp, vp, ks, vs)
+    return lib.sl_kv_append(ref, kn, vn, bt, lens, kp, vp)
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+def test_append_rejects_bad_arguments(lib, fp8):
+    """KV append validates before touching the GPU: nulls, shapes, alignment; batch 0 is a no-op."""
+    assert _append(lib, None, fp8) == -1
+    d = _desc()
+    assert _append(lib, d, fp8, kn=None) == -1
+    assert _append(lib, d, fp8, vp=None) == -1
+    assert _append(lib, d, fp8, kn=FAKE + 2) == -6
+    assert _append(lib, d, fp8, kp=FAKE + 4) == -6
+    assert _append(lib, d, fp8, lens=FAKE + 1) == -6
+    if fp8:
+        assert _append(lib, d, fp8, ks=None) == -1
+        assert _append(lib, d, fp8, vs=FAKE + 2) == -6
+    assert _append(lib, _desc(head_dim=96), fp8) == -3
+    assert _append(lib, _desc(page_size=8), fp8) == -3
+    assert _append(lib, _desc(num_kv_heads=3), fp8) == -2
+    assert _append(lib, _desc(batch=0), fp8, kn=None, vn=None, bt=None, lens=None, kp=None, vp=None,
+                   ks=None, vs=None) == 0
