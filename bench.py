@@ -48,6 +48,16 @@ def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int,
     return kv + scales + qo + table
 
 
+def append_bytes(seq_lens: np.ndarray, num_kv_heads: int, head_dim: int, kv_bytes: int) -> int:
+    """Algorithmic bytes of one KV append: the new K and V rows (bf16) read, their cached form
+    written, the per-(page, head) scales read and written (E4M3), and one length and one
+    block-table entry per appending sequence. Re-encoded earlier rows are not counted."""
+    n = int((seq_lens >= 1).sum())
+    rows = n * num_kv_heads * 2 * head_dim * (2 + kv_bytes)
+    scales = n * num_kv_heads * 2 * 8 if kv_bytes == 1 else 0
+    return rows + scales + n * 8
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
@@ -276,6 +286,51 @@ def main(argv=None) -> int:
             "kernel_source_sha": kernel_source_hash(),
         },
     }
+    # KV append (the step before attention) and the whole decode step (append +
+    # attention). The new rows overwrite each sequence's newest slot, so
+    # repeating the step leaves the sequence lengths and the bytes unchanged.
+    print(f"[bench] kv append + decode step, {args.steps} steps", file=sys.stderr, flush=True)
+    gen = torch.Generator(device=dev).manual_seed(args.seed + 7)
+    B, Hq, D = batch.q.shape
+    Hkv = batch.k_pages.shape[1]
+    k_new = torch.randn((B, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+    v_new = torch.randn((B, Hkv, D), generator=gen, device=dev).to(torch.bfloat16)
+    fp8_kw = dict(k_scales=batch.k_scales, v_scales=batch.v_scales) if kvb == 1 else {}
+
+    def append(timing=None):
+        sl.kv_append(k_new, v_new, batch.block_table, batch.seq_lens, batch.k_pages, batch.v_pages,
+                     num_q_heads=Hq, timing=timing, **fp8_kw)
+
+    for _ in range(args.warmup):
+        append()
+        sl.run_batch(batch, out=out, num_workers=args.workers)
+    torch.cuda.synchronize()
+    d0 = torch.cuda.Event(enable_timing=True)
+    d1 = torch.cuda.Event(enable_timing=True)
+    d0.record()
+    for _ in range(args.steps):
+        append()
+        sl.run_batch(batch, out=out, num_workers=args.workers)
+    d1.record()
+    torch.cuda.synchronize()
+    decode_ms = d0.elapsed_time(d1) / args.steps
+    for i in range(args.steps):
+        append(timing=(starts[i].cuda_event, stops[i].cuda_event))
+    torch.cuda.synchronize()
+    app_ms = float(np.mean([s.elapsed_time(e) for s, e in zip(starts, stops)]))
+    app_bytes = append_bytes(L, Hkv, D, kvb)
+    result["kv_append"] = {
+        "kernel": "append_kernel", "bound": "latency", "kernel_ms": round(app_ms, 5),
+        "algorithmic_bytes_per_launch": app_bytes,
+        "achieved": round(app_bytes / (app_ms * 1e-3) / 1e9, 2), "unit": "GB/s",
+        "frac_of_hbm_peak": round(app_bytes / (app_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 5),
+    }
+    result["decode_step"] = {
+        "what": "kv append + decode attention, one layer", "ms_per_step": round(decode_ms, 5),
+        "steps_per_s": round(1e3 / decode_ms, 2),
+        "GBps": round((nbytes + app_bytes) / (decode_ms * 1e-3) / 1e9, 2),
+    }
+
     if args.cpu_seconds > 0:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(batch, out, args.cpu_seconds)
