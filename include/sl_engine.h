@@ -1,0 +1,114 @@
+/*
+ * libsl decode engine: a multi-step generation loop on one GPU, driving the
+ * KV append and decode-attention kernels of sl.h for a whole set of samples.
+ *
+ * What it runs (StreamRL Section 5.3, "Scheduling Order", and Section 6). An
+ * instance holds more samples than its batch size BS, so generation runs in
+ * rounds: the batch is BS slots, each decode step every occupied slot
+ * generates one token, a sample occupies its slot for as many steps as it
+ * has output tokens, and a finished sample is released at once (continuous
+ * batching). Samples are admitted longest-first by their estimated output
+ * length (LPT); whenever a sample finishes, the next sample in that order
+ * takes the freed slot. Readings where the paper is silent: ties keep index
+ * order; freed slots are refilled before the next step, lowest slot first;
+ * a sample's prompt of p tokens is present in the cache when it is admitted
+ * (prefill is not part of this engine; the prompt pages are filled with
+ * synthetic values); while generating its k-th token (k = 1..o) the sample's
+ * sequence length is p + k.
+ *
+ * KV pages: one pool of num_pages pages of 16 tokens, handed out from a LIFO
+ * free stack that initially yields 0, 1, 2, ...; a sample takes ceil(p / 16)
+ * pages on admission and one more page in each step whose new token starts a
+ * page; a finished sample's pages return to the stack last block first.
+ *
+ * Every step, on desc.stream and in this order: the step's sequence lengths
+ * and new block-table entries are copied to the device and applied; new
+ * prompt pages are filled; sl_kv_append stores the step's new K/V rows (the
+ * caller's k_new / v_new buffers, the same every step); sl_decode_attn (or
+ * _fp8) computes the step's attention output into `out` with the caller's q.
+ * Slots without a sample have length 0 (zero output rows).
+ *
+ * The schedule is fixed by the lengths given at creation, so the host never
+ * waits for the device during a run: steps are enqueued asynchronously, and
+ * the host only waits for the copy of a staging buffer it is about to reuse.
+ *
+ * Memory: all buffers in sl_engine_buffers are the caller's; the engine keeps
+ * their pointers until sl_engine_destroy. The engine allocates, at creation
+ * only, one device staging buffer and a small ring of pinned host buffers,
+ * released by sl_engine_destroy.
+ */
+#ifndef SL_ENGINE_H
+#define SL_ENGINE_H
+
+#include "sl.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sl_engine sl_engine;
+
+typedef struct sl_engine_config {
+    int32_t num_samples;        /* M >= 1 */
+    int32_t admission;          /* 1: longest estimated output first (LPT); 0: index order (FIFO) */
+    int32_t kv_fp8;             /* 0: bf16 cache; 1: E4M3 cache with per-(page, head) scales */
+    uint32_t fill_seed;         /* seed of the synthetic prompt KV values */
+    float attn_scale;           /* softmax scale of the attention calls */
+    const int32_t *prompt_len;  /* host [M], >= 0; read during sl_engine_create only */
+    const int32_t *output_len;  /* host [M], >= 1; tokens each sample generates */
+    const int32_t *est_len;     /* host [M]; admission key for LPT */
+} sl_engine_config;
+
+typedef struct sl_engine_buffers {
+    /* batch = BS slots; heads, head_dim, page_size 16, max_blocks_per_seq,
+       num_pages, num_workers, stream and workspace as for sl_decode_attn. */
+    sl_attn_desc desc;
+    const uint16_t *q;          /* bf16 [BS][Hq][D], used every step */
+    const uint16_t *k_new;      /* bf16 [BS][Hkv][D], appended every step */
+    const uint16_t *v_new;
+    void *k_pages;              /* bf16 or E4M3 [num_pages][Hkv][16][D] */
+    void *v_pages;
+    float *k_scales;            /* E4M3 only: fp32 [num_pages][Hkv] */
+    float *v_scales;
+    int32_t *block_table;       /* [BS][max_blocks_per_seq], written by the engine */
+    int32_t *seq_lens;          /* [BS], written by the engine */
+    uint16_t *out;              /* bf16 [BS][Hq][D], the latest step's attention output */
+} sl_engine_buffers;
+
+/*
+ * Validate and build an engine: admission order, free stack, empty slots.
+ * Requires max_blocks_per_seq >= ceil((p_i + o_i) / 16) for every sample and
+ * num_pages >= BS * max_blocks_per_seq (so a page is always available).
+ * Errors: SL_ERR_NULL, SL_ERR_SHAPE (lengths, sizes), SL_ERR_UNSUPPORTED (as
+ * sl_decode_attn), SL_ERR_WORKSPACE, SL_ERR_ALIGNMENT, SL_ERR_HIP (allocation).
+ */
+sl_status sl_engine_create(const sl_engine_config *config, const sl_engine_buffers *buffers,
+                           sl_engine **engine);
+
+/*
+ * Enqueue up to max_steps further decode steps (fewer if every sample
+ * finishes); *steps_run receives the number enqueued (0 once done).
+ * Asynchronous: synchronise desc.stream before reading device buffers.
+ * Errors: SL_ERR_NULL, SL_ERR_SHAPE (max_steps < 0), SL_ERR_HIP or the
+ * status of a failing append / attention call (the engine then stops).
+ */
+sl_status sl_engine_run(sl_engine *engine, int32_t max_steps, int32_t *steps_run);
+
+/*
+ * The schedule so far (host arrays, caller-owned): per sample its slot,
+ * first and last step (-1 while not admitted / not finished); *steps the
+ * number of steps enqueued; active[s] (for s < min(*steps, active_cap), may
+ * be NULL) the number of occupied slots in step s.
+ */
+sl_status sl_engine_schedule(const sl_engine *engine, int32_t *slot, int32_t *admit_step,
+                             int32_t *finish_step, int32_t *steps, int32_t *active,
+                             int32_t active_cap);
+
+/* Wait for the engine's stream, then release its staging memory. NULL is a no-op. */
+sl_status sl_engine_destroy(sl_engine *engine);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SL_ENGINE_H */

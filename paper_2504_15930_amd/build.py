@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIBRARY = os.path.join(HERE, "libsl.so")
-SOURCES = ["partition.hip", "decode_split.hip", "merge.hip", "append.hip", "api.cpp"]
+SOURCES = ["partition.hip", "decode_split.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
+           "engine.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -1,0 +1,316 @@
+// Decode engine: the multi-step generation loop of include/sl_engine.h.
+//
+// The host owns the schedule. Samples are admitted in LPT (or index) order
+// into BS slots, pages come from a LIFO free stack, and the lengths given at
+// creation fix every step in advance. Each step is packed into a pinned
+// staging buffer ([seq_lens][block-table updates][prompt pages to fill]),
+// copied to the device asynchronously and followed by four launches on the
+// caller's stream: apply, fill (only when a prompt was admitted), KV append
+// and decode attention. A ring of pinned buffers, each reused only once the
+// copy that read it has completed, lets the host run ahead of the GPU.
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "sl.h"
+#include "sl_engine.h"
+#include "sl_internal.h"
+
+namespace {
+
+using sl::kPageSize;
+constexpr int kRing = 8;
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+}  // namespace
+
+struct sl_engine {
+    sl_engine_buffers buf{};
+    sl_attn_desc step_desc{};          // buf.desc without timing events
+    int M = 0, BS = 0, max_blocks = 0, num_pages = 0, Hkv = 0, D = 0;
+    bool fp8 = false;
+    uint32_t seed = 0;
+    float attn_scale = 0.f;
+    std::vector<int32_t> prompt, outlen;
+    std::vector<int32_t> queue;        // admission order
+    size_t head = 0;
+    std::vector<int32_t> free_stack;   // back() is popped next
+    std::vector<int32_t> occupant, made;
+    std::vector<std::vector<int32_t>> pages;
+    std::vector<int32_t> slot, admit, finish, active;
+    int step = 0;
+    bool done = false;
+    sl_status failed = SL_OK;
+    int32_t *d_stage = nullptr;
+    size_t stage_ints = 0;
+    int32_t *h_stage[kRing] = {};
+    hipEvent_t ev[kRing] = {};
+    bool ev_pending[kRing] = {};
+    int ring = 0;
+
+    void release()
+    {
+        for (int r = 0; r < kRing; ++r) {
+            if (ev[r])
+                (void)hipEventDestroy(ev[r]);
+            if (h_stage[r])
+                (void)hipHostFree(h_stage[r]);
+        }
+        if (d_stage)
+            (void)hipFree(d_stage);
+    }
+
+    sl_status one_step();
+};
+
+sl_status sl_engine::one_step()
+{
+    // Refill free slots, lowest first, taking prompt pages in block order.
+    std::vector<int32_t> upd;    // (slot, block, page) triples
+    std::vector<int32_t> fills;  // prompt pages to fill
+    for (int b = 0; b < BS; ++b) {
+        if (occupant[b] >= 0 || head >= queue.size())
+            continue;
+        const int i = queue[head++];
+        occupant[b] = i;
+        made[b] = 0;
+        slot[i] = b;
+        admit[i] = step;
+        const int n = (prompt[i] + kPageSize - 1) / kPageSize;
+        pages[b].clear();
+        for (int k = 0; k < n; ++k) {
+            const int32_t pg = free_stack.back();
+            free_stack.pop_back();
+            pages[b].push_back(pg);
+            upd.insert(upd.end(), {b, k, pg});
+            fills.push_back(pg);
+        }
+    }
+    int n_active = 0;
+    for (int b = 0; b < BS; ++b)
+        n_active += occupant[b] >= 0;
+    if (n_active == 0) {
+        done = true;
+        return SL_OK;
+    }
+
+    // This step's lengths, and a new page for every token that opens one.
+    const int r = ring;
+    ring = (ring + 1) % kRing;
+    if (ev_pending[r] && hipEventSynchronize(ev[r]) != hipSuccess)
+        return SL_ERR_HIP;
+    int32_t *h = h_stage[r];
+    for (int b = 0; b < BS; ++b) {
+        const int i = occupant[b];
+        if (i < 0) {
+            h[b] = 0;
+            continue;
+        }
+        const int t = prompt[i] + made[b];   // position of this step's token
+        if (t % kPageSize == 0) {
+            const int32_t pg = free_stack.back();
+            free_stack.pop_back();
+            pages[b].push_back(pg);
+            upd.insert(upd.end(), {b, t / kPageSize, pg});
+        }
+        h[b] = t + 1;
+    }
+    const int n_upd = (int)upd.size() / 3;
+    const int n_fill = (int)fills.size();
+    std::memcpy(h + BS, upd.data(), sizeof(int32_t) * upd.size());
+    std::memcpy(h + BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
+    const size_t ints = BS + upd.size() + fills.size();
+    hipStream_t s = step_desc.stream;
+    if (hipMemcpyAsync(d_stage, h, sizeof(int32_t) * ints, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipEventRecord(ev[r], s) != hipSuccess)
+        return SL_ERR_HIP;
+    ev_pending[r] = true;
+    if (sl::launch_engine_apply(d_stage, BS, n_upd, max_blocks, buf.seq_lens, buf.block_table, s) != hipSuccess)
+        return SL_ERR_HIP;
+    if (n_fill > 0 &&
+        sl::launch_engine_fill(d_stage + BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
+                               buf.k_scales, buf.v_scales, s) != hipSuccess)
+        return SL_ERR_HIP;
+    sl_status st;
+    if (fp8) {
+        st = sl_kv_append_fp8(&step_desc, buf.k_new, buf.v_new, buf.block_table, buf.seq_lens,
+                              static_cast<uint8_t *>(buf.k_pages), static_cast<uint8_t *>(buf.v_pages),
+                              buf.k_scales, buf.v_scales);
+        if (st == SL_OK)
+            st = sl_decode_attn_fp8(&step_desc, buf.q, static_cast<const uint8_t *>(buf.k_pages),
+                                    static_cast<const uint8_t *>(buf.v_pages), buf.k_scales, buf.v_scales,
+                                    buf.block_table, buf.seq_lens, attn_scale, buf.out);
+    } else {
+        st = sl_kv_append(&step_desc, buf.k_new, buf.v_new, buf.block_table, buf.seq_lens,
+                          static_cast<uint16_t *>(buf.k_pages), static_cast<uint16_t *>(buf.v_pages));
+        if (st == SL_OK)
+            st = sl_decode_attn(&step_desc, buf.q, static_cast<const uint16_t *>(buf.k_pages),
+                                static_cast<const uint16_t *>(buf.v_pages), buf.block_table, buf.seq_lens,
+                                attn_scale, buf.out);
+    }
+    if (st != SL_OK)
+        return st;
+
+    // The step ran: every occupied slot made one token; finished samples
+    // leave and give their pages back, last block first.
+    active.push_back(n_active);
+    for (int b = 0; b < BS; ++b) {
+        const int i = occupant[b];
+        if (i < 0)
+            continue;
+        if (++made[b] == outlen[i]) {
+            finish[i] = step;
+            for (auto it = pages[b].rbegin(); it != pages[b].rend(); ++it)
+                free_stack.push_back(*it);
+            pages[b].clear();
+            occupant[b] = -1;
+        }
+    }
+    ++step;
+    return SL_OK;
+}
+
+extern "C" {
+
+sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers *bufs, sl_engine **out)
+{
+    if (!cfg || !bufs || !out)
+        return SL_ERR_NULL;
+    *out = nullptr;
+    const sl_attn_desc &d = bufs->desc;
+    size_t need = 0;
+    sl_status st = sl_decode_attn_workspace_size(&d, &need);   // validates the descriptor
+    if (st != SL_OK)
+        return st;
+    if (!d.workspace || d.workspace_bytes < need || !aligned(d.workspace, 256))
+        return SL_ERR_WORKSPACE;
+    const int M = cfg->num_samples, BS = d.batch;
+    if (M < 1 || BS < 1 || (cfg->admission != 0 && cfg->admission != 1))
+        return SL_ERR_SHAPE;
+    if (!cfg->prompt_len || !cfg->output_len || !cfg->est_len)
+        return SL_ERR_NULL;
+    if (!bufs->q || !bufs->k_new || !bufs->v_new || !bufs->k_pages || !bufs->v_pages || !bufs->block_table ||
+        !bufs->seq_lens || !bufs->out)
+        return SL_ERR_NULL;
+    const bool fp8 = cfg->kv_fp8 != 0;
+    if (fp8 && (!bufs->k_scales || !bufs->v_scales))
+        return SL_ERR_NULL;
+    if (!aligned(bufs->q, 16) || !aligned(bufs->out, 16) || !aligned(bufs->k_pages, 16) ||
+        !aligned(bufs->v_pages, 16) || !aligned(bufs->k_new, 4) || !aligned(bufs->v_new, 4) ||
+        !aligned(bufs->block_table, 4) || !aligned(bufs->seq_lens, 4) ||
+        (fp8 && (!aligned(bufs->k_scales, 4) || !aligned(bufs->v_scales, 4))))
+        return SL_ERR_ALIGNMENT;
+    int max_prompt_blocks = 0;
+    for (int i = 0; i < M; ++i) {
+        const long long p = cfg->prompt_len[i], o = cfg->output_len[i];
+        if (p < 0 || o < 1 || (p + o + kPageSize - 1) / kPageSize > d.max_blocks_per_seq)
+            return SL_ERR_SHAPE;
+        max_prompt_blocks = std::max(max_prompt_blocks, (int)((p + kPageSize - 1) / kPageSize));
+    }
+    if ((long long)d.num_pages < (long long)BS * d.max_blocks_per_seq)
+        return SL_ERR_SHAPE;
+
+    sl_engine *e = new (std::nothrow) sl_engine;
+    if (!e)
+        return SL_ERR_HIP;
+    e->buf = *bufs;
+    e->step_desc = d;
+    e->step_desc.timing_start = nullptr;
+    e->step_desc.timing_stop = nullptr;
+    e->M = M;
+    e->BS = BS;
+    e->max_blocks = d.max_blocks_per_seq;
+    e->num_pages = d.num_pages;
+    e->Hkv = d.num_kv_heads;
+    e->D = d.head_dim;
+    e->fp8 = fp8;
+    e->seed = cfg->fill_seed;
+    e->attn_scale = cfg->attn_scale;
+    e->prompt.assign(cfg->prompt_len, cfg->prompt_len + M);
+    e->outlen.assign(cfg->output_len, cfg->output_len + M);
+    e->queue.resize(M);
+    for (int i = 0; i < M; ++i)
+        e->queue[i] = i;
+    if (cfg->admission == 1) {
+        const int32_t *est = cfg->est_len;
+        std::stable_sort(e->queue.begin(), e->queue.end(), [est](int a, int b) { return est[a] > est[b]; });
+    }
+    e->free_stack.resize(d.num_pages);
+    for (int k = 0; k < d.num_pages; ++k)
+        e->free_stack[k] = d.num_pages - 1 - k;   // pops 0, 1, 2, ...
+    e->occupant.assign(BS, -1);
+    e->made.assign(BS, 0);
+    e->pages.assign(BS, {});
+    e->slot.assign(M, -1);
+    e->admit.assign(M, -1);
+    e->finish.assign(M, -1);
+    // staging: lengths, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
+    e->stage_ints = (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
+    bool ok = hipMalloc(&e->d_stage, sizeof(int32_t) * e->stage_ints) == hipSuccess;
+    for (int r = 0; ok && r < kRing; ++r)
+        ok = hipHostMalloc(reinterpret_cast<void **>(&e->h_stage[r]), sizeof(int32_t) * e->stage_ints,
+                           hipHostMallocDefault) == hipSuccess &&
+             hipEventCreateWithFlags(&e->ev[r], hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+        e->release();
+        delete e;
+        return SL_ERR_HIP;
+    }
+    *out = e;
+    return SL_OK;
+}
+
+sl_status sl_engine_run(sl_engine *e, int32_t max_steps, int32_t *steps_run)
+{
+    if (!e || !steps_run)
+        return SL_ERR_NULL;
+    if (max_steps < 0)
+        return SL_ERR_SHAPE;
+    *steps_run = 0;
+    if (e->failed != SL_OK)
+        return e->failed;
+    for (int k = 0; k < max_steps && !e->done; ++k) {
+        const int before = e->step;
+        const sl_status st = e->one_step();
+        if (st != SL_OK) {
+            e->failed = st;
+            return st;
+        }
+        *steps_run += e->step - before;
+    }
+    return SL_OK;
+}
+
+sl_status sl_engine_schedule(const sl_engine *e, int32_t *slot, int32_t *admit_step, int32_t *finish_step,
+                             int32_t *steps, int32_t *active, int32_t active_cap)
+{
+    if (!e)
+        return SL_ERR_NULL;
+    if (slot)
+        std::copy(e->slot.begin(), e->slot.end(), slot);
+    if (admit_step)
+        std::copy(e->admit.begin(), e->admit.end(), admit_step);
+    if (finish_step)
+        std::copy(e->finish.begin(), e->finish.end(), finish_step);
+    if (steps)
+        *steps = e->step;
+    if (active && active_cap > 0) {
+        const size_t n = std::min((size_t)active_cap, e->active.size());
+        std::copy(e->active.begin(), e->active.begin() + n, active);
+    }
+    return SL_OK;
+}
+
+sl_status sl_engine_destroy(sl_engine *e)
+{
+    if (!e)
+        return SL_OK;
+    const sl_status st = hipStreamSynchronize(e->step_desc.stream) == hipSuccess ? SL_OK : SL_ERR_HIP;
+    e->release();
+    delete e;
+    return st;
+}
+
+}  // extern "C"

@@ -1,5 +1,6 @@
 // Internal interface between the host-side entry points (api.cpp) and the
-// gfx950 kernels (partition.hip, decode_split.hip, merge.hip, append.hip).
+// gfx950 kernels (partition.hip, decode_split.hip, merge.hip, append.hip,
+// engine.hip), and the decode engine (engine.cpp).
 //
 // Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
 // n_b = ceil(L_b / 16) page-head tiles (16 tokens x head_dim of one KV head).
@@ -113,6 +114,12 @@ hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);
+// Decode engine helpers (engine.hip): apply a step's lengths and block-table
+// updates from a device staging buffer; fill prompt pages with synthetic data.
+hipError_t launch_engine_apply(const int32_t *stage, int bs, int n_upd, int max_blocks, int32_t *seq_lens,
+                               int32_t *block_table, hipStream_t stream);
+hipError_t launch_engine_fill(const int32_t *pages, int n_pages, int hkv, int head_dim, bool fp8, uint32_t seed,
+                              void *k_pages, void *v_pages, float *k_scales, float *v_scales, hipStream_t stream);
 // Resident split-kernel workgroups per CU (occupancy query), for the default worker count.
 hipError_t split_blocks_per_cu(int head_dim, bool fp8, int *blocks);
 

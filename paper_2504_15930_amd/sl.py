@@ -20,6 +20,8 @@ STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_U
                 -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
            "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_status_string"]
+# include/sl_engine.h (typed in engine.py)
+ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
 
 
 class SlError(RuntimeError):

@@ -1,6 +1,7 @@
 """The C ABI on the host: the library loads, exports what include/sl.h declares,
 and rejects bad arguments before touching the GPU (no compute calls here)."""
 import ctypes
+import glob
 import os
 import re
 
@@ -10,13 +11,15 @@ import torch
 from paper_2504_15930_amd import sl
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "sl.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(sl_[a-z0-9_]+)\s*\(", text)))
+    names = set()
+    for header in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(header).read(), flags=re.S)
+        names |= set(re.findall(r"\b(sl_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -29,7 +32,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert set(names) == set(sl.EXPORTS), names
+    assert set(names) == set(sl.EXPORTS) | set(sl.ENGINE_EXPORTS), names
     for name in names:
         assert hasattr(lib, name), name
 
@@ -152,3 +155,22 @@ def test_append_rejects_bad_arguments(lib, fp8):
     assert _append(lib, _desc(num_kv_heads=3), fp8) == -2
     assert _append(lib, _desc(batch=0), fp8, kn=None, vn=None, bt=None, lens=None, kp=None, vp=None,
                    ks=None, vs=None) == 0
+
+
+def test_engine_rejects_bad_arguments(lib):
+    """The engine validates its configuration before allocating anything."""
+    from paper_2504_15930_amd import engine as E
+    E._lib()
+    handle = ctypes.c_void_p()
+    lens = (ctypes.c_int32 * 2)(10, 20)
+    outs = (ctypes.c_int32 * 2)(5, 6)
+    cfg = E.Config(2, 1, 0, 0, 0.125, ctypes.addressof(lens), ctypes.addressof(outs), ctypes.addressof(outs))
+    bufs = E.Buffers(_desc(batch=2, max_blocks=4, num_pages=8), *([FAKE] * 10))
+    assert lib.sl_engine_create(None, ctypes.byref(bufs), ctypes.byref(handle)) == -1
+    assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(bufs), None) == -1
+    assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(bufs), ctypes.byref(handle)) == -4  # no workspace
+    bad = E.Buffers(_desc(batch=2, head_dim=96), *([FAKE] * 10))
+    assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(bad), ctypes.byref(handle)) == -3
+    n = ctypes.c_int32(0)
+    assert lib.sl_engine_run(None, 1, ctypes.byref(n)) == -1
+    assert lib.sl_engine_destroy(None) == 0
