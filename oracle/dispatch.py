@@ -28,7 +28,8 @@ Readings where the paper is silent or ambiguous:
     min(M, max_batch), max_batch standing for the KV-memory limit the paper
     mentions; Equation 2 is 0 for an empty group;
   * PTL between profiled batch sizes is linear interpolation; below the first
-    point it is the first value, beyond the last it continues the last segment;
+    point it is the first value, beyond the last it continues the last segment
+    (a single profiled point gives a flat curve);
   * a group with samples needs at least one instance, an empty group may get
     none; splits are visited with N_l ascending and the first minimum is kept;
   * combining the two groups: Algorithm 2 adds the two latencies
@@ -54,7 +55,7 @@ def ptl(batch: int, table_batch, table_seconds) -> float:
     """Per-token latency at ``batch`` from profiled points (piecewise linear)."""
     xs = [int(x) for x in table_batch]
     ys = [float(y) for y in table_seconds]
-    if batch <= xs[0]:
+    if batch <= xs[0] or len(xs) == 1:      # one profiled point: a flat curve
         return ys[0]
     for k in range(1, len(xs)):
         if batch <= xs[k]:

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIBRARY = os.path.join(HERE, "libsl.so")
 SOURCES = ["partition.hip", "decode_split.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
-           "engine.cpp"]
+           "engine.cpp", "dispatch.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -22,6 +22,8 @@ EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_de
            "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_status_string"]
 # include/sl_engine.h (typed in engine.py)
 ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
+# include/sl_dispatch.h (typed in dispatch.py)
+DISPATCH_EXPORTS = ["sl_generation_latency", "sl_dispatch_plan"]
 
 
 class SlError(RuntimeError):
