@@ -392,8 +392,11 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
     if (w >= p.num_workers)
         return;
     const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
-    const long long s0 = (long long)w * total / p.num_workers;
-    const long long s1 = (long long)(w + 1) * total / p.num_workers;
+    const int nw = effective_workers(total, p.num_workers);
+    if (w >= nw)
+        return;
+    const long long s0 = (long long)w * total / nw;
+    const long long s1 = (long long)(w + 1) * total / nw;
     if (s0 >= s1)
         return;
     const int ntiles = (int)(s1 - s0);

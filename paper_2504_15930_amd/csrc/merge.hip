@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p)
         return;
     }
     const long long total = (long long)p.cum_pages[p.batch] * Hkv;
-    const long long NW = p.num_workers;
+    const long long NW = effective_workers(total, p.num_workers);
     const long long a = (long long)Hkv * cb + (long long)g * nb;   // first tile of the unit
     const long long e = a + nb;                                    // one past its last tile
     // Worker holding tile x: the largest w with floor(w * total / NW) <= x.

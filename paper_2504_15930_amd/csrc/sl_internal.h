@@ -38,6 +38,21 @@ constexpr int kMaxBatch = 8192;            // the partitioner keeps one int per 
 constexpr int kPartitionThreads = 1024;
 constexpr int kMergeThreads = 256;         // one wave per unit, four units per block
 constexpr int kMaxWorkers = 1 << 16;       // keeps partial-state offsets below 2^31 bytes
+#ifndef SL_MIN_TILES_PER_WORKER
+#define SL_MIN_TILES_PER_WORKER 8
+#endif
+// A worker is given at least this many tiles: a small stream (a small batch, a
+// short context) is split over fewer workers rather than cut into pieces of
+// one or two tiles, each of which would cost a partial state and a merge step.
+constexpr int kMinTilesPerWorker = SL_MIN_TILES_PER_WORKER;
+
+// Workers that take part in a stream of `total` tiles (the others exit at
+// once); both the split kernel and the merge derive it from the same total.
+__host__ __device__ inline int effective_workers(long long total, int num_workers)
+{
+    const long long want = (total + kMinTilesPerWorker - 1) / kMinTilesPerWorker;
+    return want < 1 ? 1 : (want < num_workers ? (int)want : num_workers);
+}
 constexpr size_t kAlign = 256;
 
 // Tile entry. `page` = page_id * Hkv + g, the index of the tile in the
