@@ -97,6 +97,89 @@ def generation(w, fp8: bool, seed: int, dev) -> dict:
     return res
 
 
+def dispatch_experiment(w, seed: int, dev) -> dict:
+    """Skewness-aware dispatching (Algorithm 2) fed by PTL(BS) measured here, against random
+    dispatch, with the generation stage of each plan measured on the decode engine.
+
+    PTL(BS): one decode step (KV append + attention, this workload's heads) over BS sequences of
+    2048 cached tokens, for BS = 1 .. 256. Batch: 1024 prompts (256-768 tokens), true output
+    lengths lognormal (median 1024, sigma 1, capped at 8192), estimates = truth times a lognormal
+    error (sigma 0.3), the length distribution D a separate draw; N = 8 instances, alpha = 0.2,
+    at most 128 sequences per instance. An instance runs its samples on the engine (LPT inside).
+    Instances are independent, so the stage time of a plan is its most loaded instance: the
+    first instance of each group (it receives the longest sample of the group) for the
+    skewness-aware plans, the instances holding the longest sample and the most tokens for the
+    random one."""
+    import torch
+
+    from paper_2504_15930_amd import dispatch as Dsp
+    from paper_2504_15930_amd import engine as E
+    from paper_2504_15930_amd import inputs, sl
+
+    Hq, Hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+    prof_b = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+    prof_s = []
+    for bs in prof_b:
+        b = inputs.make_paged_batch([2048] * bs, Hq, Hkv, D, seed=seed + 1, device=dev, poison=False)
+        kn = torch.randn((bs, Hkv, D), device=dev).to(torch.bfloat16)
+        out = torch.empty_like(b.q)
+        for it in range(35):
+            if it == 5:
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+            sl.kv_append(kn, kn, b.block_table, b.seq_lens, b.k_pages, b.v_pages, num_q_heads=Hq)
+            sl.run_batch(b, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        prof_s.append(e0.elapsed_time(e1) / 30 * 1e-3)
+        del b
+        torch.cuda.empty_cache()
+    rng = np.random.default_rng(seed)
+    P, N, alpha, maxb = 1024, 8, 0.2, 128
+    true = np.clip(np.exp(rng.normal(np.log(1024), 1.0, P)), 16, 8192).astype(np.int32)
+    est = np.maximum(1, true * np.exp(rng.normal(0.0, 0.3, P))).astype(np.int32)
+    prompt = rng.integers(256, 769, P).astype(np.int32)
+    dist = np.clip(np.exp(rng.normal(np.log(1024), 1.0, 1024)), 16, 8192).astype(np.int32)
+
+    def run(sel):
+        idx = np.nonzero(sel)[0]
+        eng = E.Engine(prompt[idx], true[idx], est[idx], batch_slots=min(len(idx), maxb), num_q_heads=Hq,
+                       num_kv_heads=Hkv, head_dim=D, lpt=True, seed=seed, device=dev)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        eng.run()
+        e1.record()
+        torch.cuda.synchronize()
+        eng.close()
+        del eng
+        torch.cuda.empty_cache()
+        return round(e0.elapsed_time(e1), 2)
+
+    res = {"ptl_profile": {"batch": prof_b, "us": [round(x * 1e6, 2) for x in prof_s],
+                           "what": "KV append + decode attention, 2048 cached tokens per sequence"},
+           "prompts": P, "instances": N, "alpha": alpha, "max_batch": maxb}
+    measured = {}
+    for combine in ("sum", "max"):
+        print(f"[bench] dispatch plan ({combine})", file=sys.stderr, flush=True)
+        nl, nr, lat, inst = Dsp.plan(est, alpha, dist, N, prof_b, prof_s, maxb, combine)
+        if (nl, nr) not in measured:
+            measured[(nl, nr)] = max(run(inst == 0), run(inst == nl))
+        res[f"plan_{combine}"] = {"long_tail_instances": nl, "regular_instances": nr,
+                                  "estimated_ms": round(lat * 1e3, 2), "measured_stage_ms": measured[(nl, nr)]}
+    print("[bench] random dispatch", file=sys.stderr, flush=True)
+    perm = np.random.default_rng(seed + 1).permutation(P)
+    rinst = np.empty(P, np.int32)
+    rinst[perm] = np.arange(P) % N
+    worst = {max(range(N), key=lambda k: true[rinst == k].max()), max(range(N), key=lambda k: true[rinst == k].sum())}
+    res["random_stage_ms"] = max(run(rinst == k) for k in sorted(worst))
+    res["speedup_sum_plan"] = round(res["random_stage_ms"] / res["plan_sum"]["measured_stage_ms"], 3)
+    res["speedup_max_plan"] = round(res["random_stage_ms"] / res["plan_max"]["measured_stage_ms"], 3)
+    return res
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
@@ -203,6 +286,8 @@ def main(argv=None) -> int:
                     help="target CPU time of the oracle baseline (0 disables it)")
     ap.add_argument("--generation", type=int, default=1,
                     help="also run a whole long-tail generation (decode engine, LPT vs FIFO admission); 0 skips it")
+    ap.add_argument("--dispatch", type=int, default=1,
+                    help="also run skewness-aware against random dispatching on the decode engine; 0 skips it")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="instead of the benchmark, run `steps` plain device-to-device copies of "
                          "BYTES bytes (the reference kernel for scaling HBM counters)")
@@ -374,6 +459,8 @@ def main(argv=None) -> int:
 
     if args.generation:
         result["generation"] = generation(w, batch.kv_dtype == "e4m3", args.seed, dev)
+    if args.dispatch:
+        result["dispatch"] = dispatch_experiment(w, args.seed, dev)
 
     if args.cpu_seconds > 0:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
