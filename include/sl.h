@@ -146,6 +146,40 @@ sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q,
                              float scale, uint16_t *out);
 
 /*
+ * Decode attention with prefix sharing (bf16 cache): the same result as
+ * sl_decode_attn, reading each page that several sequences share only once.
+ * StreamRL's engine shares key-value cache between samples of one prompt
+ * (Section 6, prefix sharing); here the samples of a group are run together
+ * over the group's shared pages.
+ *
+ * Groups are runs of consecutive sequences: group k is sequences
+ * [group_start[k], group_start[k+1]), and their first shared_pages[k] pages
+ * are the same, i.e. block_table[b][i] == block_table[group_start[k]][i] for
+ * i < shared_pages[k] and every member b (only the first member's entries are
+ * read), and seq_lens[b] >= 16 * shared_pages[k]. Sequences in no group, or in
+ * a group with shared_pages 0, are attended as by sl_decode_attn.
+ *   group_start   device int32 [num_groups + 1], ascending, within [0, batch]
+ *   shared_pages  device int32 [num_groups]
+ *   num_groups    0 .. batch (0: plain attention, in two passes)
+ * A group with more than min(16, 64 / (Hq / Hkv)) members, or whose range or
+ * page count is out of bounds, is treated as unshared (exact, without the
+ * saving). A member shorter than its group's shared pages gets NaN rows.
+ * Everything else is as sl_decode_attn; batch is at most 4096, and the
+ * workspace is sized by sl_decode_attn_prefix_workspace_size.
+ * Errors: as sl_decode_attn (SL_ERR_SHAPE also for num_groups outside
+ * [0, batch]; SL_ERR_UNSUPPORTED for batch > 4096).
+ */
+sl_status sl_decode_attn_prefix(const sl_attn_desc *desc, const uint16_t *q,
+                                const uint16_t *k_pages, const uint16_t *v_pages,
+                                const int32_t *block_table, const int32_t *seq_lens,
+                                const int32_t *group_start, const int32_t *shared_pages,
+                                int32_t num_groups, float scale, uint16_t *out);
+
+/* Workspace bytes sl_decode_attn_prefix needs for desc and num_groups. */
+sl_status sl_decode_attn_prefix_workspace_size(const sl_attn_desc *desc, int32_t num_groups,
+                                               size_t *bytes);
+
+/*
  * KV append: stores one decode step's new key and value rows in the paged
  * cache, the step that precedes attention in every decode step (StreamRL,
  * Section 2.1: each decoding step computes the newest token and keeps its

@@ -32,6 +32,37 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
     return off;
 }
 
+size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
+                               int head_dim, int num_workers, int num_groups, PrefixWorkspace *ws)
+{
+    char *p = static_cast<char *>(base);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char *r = p ? p + off : nullptr;
+        off += align_up(bytes);
+        return r;
+    };
+    PrefixWorkspace w;
+    w.cum_own = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
+    w.seq_group = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)batch));
+    w.cum_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)num_groups + 1)));
+    w.own_tiles = reinterpret_cast<TileEntry *>(take(sizeof(TileEntry) * (size_t)batch * max_blocks * num_kv_heads));
+    w.shared_tiles =
+        reinterpret_cast<TileEntry *>(take(sizeof(TileEntry) * (size_t)num_groups * max_blocks * num_kv_heads));
+    w.own_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
+    w.own_acc = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
+    w.shared_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * kPrefixRows * 2));
+    w.shared_acc = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * kPrefixRows * head_dim));
+    const size_t units = (size_t)batch * num_kv_heads;
+    w.own_unit_ml = reinterpret_cast<float *>(take(sizeof(float) * units * group * 2));
+    w.own_unit_acc = reinterpret_cast<float *>(take(sizeof(float) * units * group * head_dim));
+    w.shared_unit_ml = reinterpret_cast<float *>(take(sizeof(float) * units * kPrefixRows * 2));
+    w.shared_unit_acc = reinterpret_cast<float *>(take(sizeof(float) * units * kPrefixRows * head_dim));
+    if (ws)
+        *ws = w;
+    return off;
+}
+
 namespace {
 
 constexpr int kMaxDevices = 64;
@@ -178,6 +209,9 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     sp.group = G;
     sp.num_workers = nw;
     sp.scale_log2 = scale * 1.4426950408889634f;
+    sp.num_q_heads = d->num_q_heads;
+    sp.unit_ml = nullptr;
+    sp.unit_acc = nullptr;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (launch_split(sp, d->head_dim, fp8, d->stream) != hipSuccess)
@@ -236,6 +270,131 @@ sl_status run_append(const sl_attn_desc *d, const uint16_t *k_new, const uint16_
     if (launch_append(ap, d->head_dim, fp8, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    return SL_OK;
+}
+
+sl_status check_prefix(const sl_attn_desc *d, int32_t num_groups)
+{
+    sl_status st = check_desc(d);
+    if (st != SL_OK)
+        return st;
+    if (num_groups < 0 || num_groups > d->batch)
+        return SL_ERR_SHAPE;
+    if (d->batch > kMaxPrefixBatch)
+        return SL_ERR_UNSUPPORTED;
+    return SL_OK;
+}
+
+sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k_pages, const uint16_t *v_pages,
+                     const int32_t *block_table, const int32_t *seq_lens, const int32_t *group_start,
+                     const int32_t *shared_pages, int32_t num_groups, float scale, uint16_t *out)
+{
+    sl_status st = check_prefix(d, num_groups);
+    if (st != SL_OK)
+        return st;
+    if (d->batch == 0)
+        return SL_OK;
+    if (!q || !k_pages || !v_pages || !block_table || !seq_lens || !out ||
+        (num_groups > 0 && (!group_start || !shared_pages)))
+        return SL_ERR_NULL;
+    if (!aligned16(q) || !aligned16(out) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned4(block_table) ||
+        !aligned4(seq_lens) || (num_groups > 0 && (!aligned4(group_start) || !aligned4(shared_pages))))
+        return SL_ERR_ALIGNMENT;
+    int nw = 0;
+    st = resolve_workers(d, false, &nw);
+    if (st != SL_OK)
+        return st;
+    const int G = d->num_q_heads / d->num_kv_heads;
+    PrefixWorkspace ws;
+    const size_t need = prefix_workspace_layout(d->workspace, d->batch, d->max_blocks_per_seq, d->num_kv_heads, G,
+                                                d->head_dim, nw, num_groups, &ws);
+    if (!d->workspace || d->workspace_bytes < need || (reinterpret_cast<uintptr_t>(d->workspace) & (kAlign - 1)) != 0)
+        return SL_ERR_WORKSPACE;
+    // With no groups the group arrays are never read; point them at the workspace.
+    const int32_t *gs = num_groups > 0 ? group_start : ws.cum_shared;
+    const int32_t *sp = num_groups > 0 ? shared_pages : ws.cum_shared;
+
+    PrefixPartitionParams pp;
+    pp.seq_lens = seq_lens;
+    pp.block_table = block_table;
+    pp.group_start = gs;
+    pp.shared_pages = sp;
+    pp.cum_own = ws.cum_own;
+    pp.cum_shared = ws.cum_shared;
+    pp.seq_group = ws.seq_group;
+    pp.own_tiles = ws.own_tiles;
+    pp.shared_tiles = ws.shared_tiles;
+    pp.batch = d->batch;
+    pp.num_groups = num_groups;
+    pp.num_q_heads = d->num_q_heads;
+    pp.num_kv_heads = d->num_kv_heads;
+    pp.max_blocks = d->max_blocks_per_seq;
+    pp.num_pages = d->num_pages;
+    if (launch_partition_prefix(pp, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+
+    SplitParams sp_;
+    sp_.q = q;
+    sp_.k_pages = k_pages;
+    sp_.v_pages = v_pages;
+    sp_.k_scales = nullptr;
+    sp_.v_scales = nullptr;
+    sp_.out = out;
+    sp_.num_kv_heads = d->num_kv_heads;
+    sp_.group = G;
+    sp_.num_workers = nw;
+    sp_.num_q_heads = d->num_q_heads;
+    sp_.scale_log2 = scale * 1.4426950408889634f;
+    // shared pass
+    sp_.tiles = ws.shared_tiles;
+    sp_.cum_pages = ws.cum_shared;
+    sp_.batch = num_groups;
+    sp_.part_ml = ws.shared_ml;
+    sp_.part_acc = ws.shared_acc;
+    sp_.unit_ml = ws.shared_unit_ml;
+    sp_.unit_acc = ws.shared_unit_acc;
+    if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (launch_split_shared(sp_, d->head_dim, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    // own pass
+    sp_.tiles = ws.own_tiles;
+    sp_.cum_pages = ws.cum_own;
+    sp_.batch = d->batch;
+    sp_.part_ml = ws.own_ml;
+    sp_.part_acc = ws.own_acc;
+    sp_.unit_ml = ws.own_unit_ml;
+    sp_.unit_acc = ws.own_unit_acc;
+    if (launch_split(sp_, d->head_dim, false, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+
+    PrefixMergeParams mp;
+    mp.seq_lens = seq_lens;
+    mp.group_start = gs;
+    mp.shared_pages = sp;
+    mp.cum_own = ws.cum_own;
+    mp.cum_shared = ws.cum_shared;
+    mp.seq_group = ws.seq_group;
+    mp.own_ml = ws.own_ml;
+    mp.own_acc = ws.own_acc;
+    mp.shared_ml = ws.shared_ml;
+    mp.shared_acc = ws.shared_acc;
+    mp.own_unit_ml = ws.own_unit_ml;
+    mp.own_unit_acc = ws.own_unit_acc;
+    mp.shared_unit_ml = ws.shared_unit_ml;
+    mp.shared_unit_acc = ws.shared_unit_acc;
+    mp.out = out;
+    mp.batch = d->batch;
+    mp.num_groups = num_groups;
+    mp.num_q_heads = d->num_q_heads;
+    mp.num_kv_heads = d->num_kv_heads;
+    mp.group = G;
+    mp.num_workers = nw;
+    mp.max_blocks = d->max_blocks_per_seq;
+    if (launch_merge_prefix(mp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     return SL_OK;
 }
@@ -327,6 +486,36 @@ const char *sl_status_string(sl_status status)
     case SL_ERR_ALIGNMENT: return "q, out or a page pool not 16-byte aligned, or an int/scale array not 4-byte aligned";
     }
     return "unknown status";
+}
+
+}  // extern "C"
+
+extern "C" {
+
+sl_status sl_decode_attn_prefix_workspace_size(const sl_attn_desc *desc, int32_t num_groups, size_t *bytes)
+{
+    sl_status st = sl::check_prefix(desc, num_groups);
+    if (st != SL_OK)
+        return st;
+    if (!bytes)
+        return SL_ERR_NULL;
+    int nw = 0;
+    st = sl::resolve_workers(desc, false, &nw);
+    if (st != SL_OK)
+        return st;
+    *bytes = sl::prefix_workspace_layout(nullptr, desc->batch, desc->max_blocks_per_seq, desc->num_kv_heads,
+                                         desc->num_q_heads / desc->num_kv_heads, desc->head_dim, nw, num_groups,
+                                         nullptr);
+    return SL_OK;
+}
+
+sl_status sl_decode_attn_prefix(const sl_attn_desc *desc, const uint16_t *q, const uint16_t *k_pages,
+                                const uint16_t *v_pages, const int32_t *block_table, const int32_t *seq_lens,
+                                const int32_t *group_start, const int32_t *shared_pages, int32_t num_groups,
+                                float scale, uint16_t *out)
+{
+    return sl::run_prefix(desc, q, k_pages, v_pages, block_table, seq_lens, group_start, shared_pages, num_groups,
+                          scale, out);
 }
 
 }  // extern "C"

@@ -36,6 +36,8 @@
 // (v_cvt_scalef32_pk_bf16_fp8 with unit scale), the per-(page, head) key
 // scale multiplies the fp32 scores and the value scale multiplies the
 // probabilities before they are rounded for the value MFMA.
+#include <type_traits>
+
 #include "sl_internal.h"
 
 namespace sl {
@@ -106,14 +108,14 @@ __device__ __forceinline__ float quad_sum(float x)
     return x + __shfl_xor(x, 32, kWave);
 }
 
-template <int D, bool FP8>
+template <int D, bool FP8, int CB = 1>
 struct Tile {
     // Per-lane dwords of K (score-MFMA A operands) and V (four rows).
     static constexpr int KW = FP8 ? D / 16 : D / 8;
     static constexpr int VW = FP8 ? D / 16 : D / 8;
     uint32_t k[KW];
     uint32_t v[VW];
-    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only
+    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only (CB == 1)
     float scl;           // FP8: key scale in lanes 0-31, value scale in lanes 32-63
     uint32_t meta;       // TileEntry::meta (wave-uniform)
     bool bad_page;       // the block table named a page outside the pool
@@ -127,8 +129,8 @@ __device__ __forceinline__ int q_index(int s, int quad)
 }
 
 // Issue every load of one tile. All loads are unconditional.
-template <int D, bool FP8>
-__device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p, int32_t page,
+template <int D, bool FP8, int CB = 1>
+__device__ __forceinline__ void issue_tile(Tile<D, FP8, CB> &t, const SplitParams &p, int32_t page,
                                            uint32_t meta, bool with_q, int n, int quad, int lane)
 {
     constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
@@ -182,10 +184,13 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     // when the operand is formed.
     if (with_q) {
         const int G = p.group;
-        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
+        if constexpr (CB == 1) {
+            const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s)
-            t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
+            for (int s = 0; s < D / 32; ++s)
+                t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
+        }
+        // (shared-prefix units load their CB query blocks when the unit starts)
     }
 }
 
@@ -195,15 +200,15 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
 // starting at quad D/64. A chunk c of row r is stored at position
 // c ^ ((r / P) % C) of its row (P rows per 256 bytes, C chunks per row), which
 // makes the 16-lane groups of both the writes and the reads hit distinct banks.
-template <int D, bool FP8>
-__device__ __forceinline__ void regroup_k(const Tile<D, FP8> &t, uint8_t *lds, int lane, int n, int quad,
+template <int D, bool FP8, int CB>
+__device__ __forceinline__ void regroup_k(const Tile<D, FP8, CB> &t, uint8_t *lds, int lane, int n, int quad,
                                           u32x4_t (&kc)[FP8 ? D / 64 : D / 32])
 {
     constexpr int R = D * (FP8 ? 1 : 2);   // bytes per row
     constexpr int C = R / 16;               // 16-byte chunks per row
     constexpr int P = 256 / R;              // rows per 256 bytes
 #pragma unroll
-    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
+    for (int i = 0; i < Tile<D, FP8, CB>::KW / 4; ++i) {
         const int off = 1024 * i + 16 * lane;
         const int r = off / R, c = (off % R) / 16;
         *reinterpret_cast<u32x4_t *>(lds + r * R + 16 * (c ^ ((r / P) % C))) =
@@ -258,7 +263,7 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
                                              int valid, uint8_t *lds, int lane, int n, int quad)
 {
     u32x4_t kc[FP8 ? D / 64 : D / 32];
-    regroup_k<D, FP8>(t, lds, lane, n, quad, kc);
+    regroup_k<D, FP8, 1>(t, lds, lane, n, quad, kc);
     f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
@@ -342,10 +347,12 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
 }
 
 // Finish the current unit: normalise and write its bf16 rows if the whole unit
-// was seen (`full`), else store the partial state in slot 2w + slot_sel.
+// was seen and nothing else is merged into it (`full`), else store the partial
+// state, G rows, in slot `slot` of (part_ml, part_acc).
 template <int D>
-__device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, uint32_t row0,
-                                            bool full, bool bad, int w, int slot_sel, int n, int quad)
+__device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, uint32_t row0, bool full,
+                                            bool bad, float *part_ml, float *part_acc, size_t slot, int n,
+                                            int quad)
 {
     const int G = p.group;
     const float l = quad_sum(st.l);
@@ -370,9 +377,8 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
             *reinterpret_cast<u32x4_t *>(dst + 16 * c) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
         }
     } else {
-        const size_t slot = 2 * (size_t)w + slot_sel;
         const float poison = bad ? __builtin_nanf("") : 0.0f;
-        float *dst = p.part_acc + (slot * G + n) * D + d0;
+        float *dst = part_acc + (slot * G + n) * D + d0;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -380,12 +386,118 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
                 *reinterpret_cast<f32x4_t *>(dst + r * (D / 16) + i) =
                     f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
         if (quad == 0)   // a NaN maximum keeps the poison alive through the merge weights
-            *reinterpret_cast<f32x2_t *>(p.part_ml + (slot * G + n) * 2) =
+            *reinterpret_cast<f32x2_t *>(part_ml + (slot * G + n) * 2) =
                 f32x2_t{st.m + poison, l};
     }
 }
 
-template <int D, bool FP8>
+// ---- shared-prefix units: CB blocks of 16 query rows per tile ------------------
+
+template <int D, int CB>
+struct PieceMulti {
+    f32x4_t acc[CB][D / 16];
+    float m[CB];
+    float l[CB];
+};
+
+template <int D, int CB>
+__device__ __forceinline__ void reset(PieceMulti<D, CB> &st)
+{
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+        for (int i = 0; i < D / 16; ++i)
+            st.acc[cb][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        st.m[cb] = kNegInf;
+        st.l[cb] = 0.f;
+    }
+}
+
+// One tile of a shared-prefix unit (bf16 cache, every page full): the K and V
+// operands are formed once and feed the score and value MFMAs of all CB
+// column blocks, so each shared page is read once for all the group's rows.
+template <int D, int CB>
+__device__ __forceinline__ void compute_tile_multi(PieceMulti<D, CB> &st, const Tile<D, false, CB> &t,
+                                                   const bf16x8_t (&qop)[CB][D / 32], float score_mul,
+                                                   uint8_t *lds, int lane, int n, int quad)
+{
+    u32x4_t kc[D / 32];
+    regroup_k<D, false, CB>(t, lds, lane, n, quad, kc);
+    constexpr int RW = D / 32;   // bf16 dwords per value row
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s)
+            s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kc[s]), qop[cb][s], s4,
+                                                         0, 0, 0);
+        float sc[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            sc[r] = s4[r] * score_mul;
+        const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
+        if (mx > st.m[cb]) {
+            const float alpha = __builtin_amdgcn_exp2f(st.m[cb] - mx);
+            st.l[cb] *= alpha;
+#pragma unroll
+            for (int i = 0; i < D / 16; ++i)
+                st.acc[cb][i] *= alpha;
+            st.m[cb] = mx;
+        }
+        float pr[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m[cb]);
+        const uint32_t p01 = pack_bf16(pr[0], pr[1]);
+        const uint32_t p23 = pack_bf16(pr[2], pr[3]);
+        st.l[cb] += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
+        const i16x4_t pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
+#pragma unroll
+        for (int i = 0; i < D / 16; ++i) {
+            const int w = i >> 1;
+            uint32_t lo, hi;
+            if ((i & 1) == 0) {
+                lo = (t.v[0 * RW + w] & 0xffffu) | (t.v[1 * RW + w] << 16);
+                hi = (t.v[2 * RW + w] & 0xffffu) | (t.v[3 * RW + w] << 16);
+            } else {
+                lo = (t.v[0 * RW + w] >> 16) | (t.v[1 * RW + w] & 0xffff0000u);
+                hi = (t.v[2 * RW + w] >> 16) | (t.v[3 * RW + w] & 0xffff0000u);
+            }
+            const i16x4_t va = __builtin_bit_cast(i16x4_t, u32x2_t{lo, hi});
+            st.acc[cb][i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, st.acc[cb][i], 0, 0, 0);
+        }
+    }
+}
+
+// A shared-prefix unit always leaves partial states (each member still has
+// its own pages to merge): rows r < members * G of slot `slot` of
+// (part_ml, part_acc), kPrefixRows rows per slot.
+template <int D, int CB>
+__device__ __forceinline__ void finish_shared(PieceMulti<D, CB> &st, int rows, bool bad, float *part_ml,
+                                              float *part_acc, size_t slot, int n, int quad)
+{
+    const float poison = bad ? __builtin_nanf("") : 0.0f;
+    const int d0 = quad * (D / 4);
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+        const float l = quad_sum(st.l[cb]);
+        const int r = 16 * cb + n;
+        if (r >= rows)
+            continue;
+        float *dst = part_acc + (slot * kPrefixRows + r) * D + d0;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+            for (int i = 0; i < D / 16; i += 4)
+                *reinterpret_cast<f32x4_t *>(dst + q4 * (D / 16) + i) =
+                    f32x4_t{st.acc[cb][i][q4], st.acc[cb][i + 1][q4], st.acc[cb][i + 2][q4],
+                            st.acc[cb][i + 3][q4]} + poison;
+        if (quad == 0)
+            *reinterpret_cast<f32x2_t *>(part_ml + (slot * kPrefixRows + r) * 2) = f32x2_t{st.m[cb] + poison, l};
+    }
+}
+
+template <int D, bool FP8, int CB = 1>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
     const int w = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -444,15 +556,15 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
         first_meta[k] = meta_of(first[k]);
     }
 
-    Tile<D, FP8> buf[kNbuf];
+    Tile<D, FP8, CB> buf[kNbuf];
 #pragma unroll
     for (int k = 0; k < kNbuf - 1; ++k)
-        issue_tile<D, FP8>(buf[k], p, first_page[k], first_meta[k],
+        issue_tile<D, FP8, CB>(buf[k], p, first_page[k], first_meta[k],
                            k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane);
 
-    Piece<D> st;
-    reset<D>(st);
-    bf16x8_t qop[D / 32];   // score-MFMA B operand of the current unit (zero rows j >= G)
+    std::conditional_t<CB == 1, Piece<D>, PieceMulti<D, CB>> st;
+    reset(st);
+    bf16x8_t qop[CB][D / 32];   // score-MFMA B operands of the current unit (zero columns past its rows)
     bool started = false;   // the current unit's first tile is inside this range
     bool bad = false;
     int slot_sel = 0;
@@ -461,25 +573,59 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
         for (int k = 0; k < kNbuf; ++k) {
             const int i = i0 + k;
             const uint32_t next_meta = meta_of(ring[k]);
-            issue_tile<D, FP8>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
+            issue_tile<D, FP8, CB>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
                                (next_meta & kMetaFirst) != 0, n, quad, lane);
             ring[k] = entry(i + 2 * kNbuf - 1);
             if (i < ntiles) {
-                const Tile<D, FP8> &t = buf[k];
+                const Tile<D, FP8, CB> &t = buf[k];
                 const uint32_t meta = t.meta;
                 if (i == 0 || (meta & kMetaFirst) != 0) {
+                    if constexpr (CB == 1) {
 #pragma unroll
-                    for (int s = 0; s < D / 32; ++s)
-                        qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
+                        for (int s = 0; s < D / 32; ++s)
+                            qop[0][s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
+                    } else {
+                        // Shared-prefix unit: column c of block cb is row r = 16 cb + c, member
+                        // r / G and head r % G of the group; columns past its rows are zero.
+                        // Loaded here, once per unit, rather than carried by every tile.
+                        const int rows = ((int)(meta & 15u) + 1) * G;
+#pragma unroll
+                        for (int cb = 0; cb < CB; ++cb) {
+                            const int r = 16 * cb + n;
+                            const size_t row = (size_t)(meta >> kMetaRowShift) +
+                                               (r < rows ? (size_t)(r / G) * p.num_q_heads + (size_t)(r % G) : 0);
+                            const uint8_t *qrow = reinterpret_cast<const uint8_t *>(p.q + row * D);
+#pragma unroll
+                            for (int s = 0; s < D / 32; ++s)
+                                qop[cb][s] = __builtin_bit_cast(
+                                    bf16x8_t, r < rows ? ld128(qrow + 2 * q_index<D, FP8>(s, quad))
+                                                       : u32x4_t{0u, 0u, 0u, 0u});
+                        }
+                    }
                 }
                 started |= (meta & kMetaFirst) != 0;
                 bad |= t.bad_page || (meta & kMetaBadLen) != 0;
-                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
-                                     quad);
+                if constexpr (CB == 1)
+                    compute_tile<D, FP8>(st, t, qop[0], p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
+                                         quad);
+                else
+                    compute_tile_multi<D, CB>(st, t, qop, p.scale_log2, lds, lane, n, quad);
                 if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
-                    finish_unit<D>(p, st, meta >> kMetaRowShift, started && (meta & kMetaLast) != 0,
-                                   bad, w, slot_sel, n, quad);
-                    reset<D>(st);
+                    // A unit cut by this range leaves its piece in the worker's slot 2w + slot_sel.
+                    // A whole unit is written out, unless it still has to be merged (shared pages,
+                    // or the own pages of a sequence that has them): then its state goes to its
+                    // own slot in the unit area, indexed by (first query row) / G.
+                    const uint32_t row0 = meta >> kMetaRowShift;
+                    const bool whole = started && (meta & kMetaLast) != 0;
+                    const bool to_unit = whole && (CB > 1 || (meta & kMetaPrefixed) != 0);
+                    float *const pml = to_unit ? p.unit_ml : p.part_ml;
+                    float *const pacc = to_unit ? p.unit_acc : p.part_acc;
+                    const size_t slot = to_unit ? (size_t)(row0 / (uint32_t)G) : 2 * (size_t)w + slot_sel;
+                    if constexpr (CB == 1)
+                        finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
+                    else
+                        finish_shared<D, CB>(st, ((int)(meta & 15u) + 1) * G, bad, pml, pacc, slot, n, quad);
+                    reset(st);
                     started = false;
                     bad = false;
                     slot_sel = 1;
@@ -503,6 +649,19 @@ hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_
         hipLaunchKernelGGL((split_kv_kernel<128, true>), grid, block, 0, stream, p);
     else if (head_dim == 64 && fp8)
         hipLaunchKernelGGL((split_kv_kernel<64, true>), grid, block, 0, stream, p);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream)
+{
+    const dim3 grid((p.num_workers + kWavesPerBlock - 1) / kWavesPerBlock);
+    const dim3 block(kWave * kWavesPerBlock);
+    if (head_dim == 128)
+        hipLaunchKernelGGL((split_kv_kernel<128, false, kPrefixBlocks>), grid, block, 0, stream, p);
+    else if (head_dim == 64)
+        hipLaunchKernelGGL((split_kv_kernel<64, false, kPrefixBlocks>), grid, block, 0, stream, p);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -138,6 +138,149 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p)
     }
 }
 
+// Prefix-sharing mode: every (sequence, head) row with shared pages, or whose
+// own pages were cut across workers, combines the pieces of its group's
+// shared unit (row member * G + head of the shared partial states) with the
+// pieces of its own unit. A unit cut across workers left one piece per worker
+// in the worker slots; a unit that one worker saw whole left its state in the
+// unit area, at (first query row) / G. Rows finished by one worker with no
+// shared pages were written by the split kernel. A sequence shorter than its
+// group's shared prefix, or with an invalid length, gets a NaN row.
+template <int D>
+__global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMergeParams p)
+{
+    constexpr int E = D / kWave;
+    const int Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
+    const int item = blockIdx.x * (kMergeThreads / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    if (item >= p.batch * Hq)
+        return;
+    const int b = item / Hq;
+    const int h = item - b * Hq;
+    const int g = h / G;
+    const int hl = h - g * G;
+    const int lane = threadIdx.x & (kWave - 1);
+    uint16_t *dst = p.out + ((size_t)b * Hq + h) * D + E * lane;
+    const int L = p.seq_lens[b];
+    const int k = p.seq_group[b];
+    const int sk = k >= 0 ? p.cum_shared[k + 1] - p.cum_shared[k] : 0;
+    const int ob = p.cum_own[b + 1] - p.cum_own[b];
+    const bool bad = L < 0 || L > p.max_blocks * kPageSize || L < sk * kPageSize;
+    if (sk == 0 && ob == 0) {
+        const uint16_t fill = L < 0 ? 0x7fc0 : 0x0000;   // bf16 NaN / +0
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            dst[e] = fill;
+        return;
+    }
+    const long long tot_o = (long long)p.cum_own[p.batch] * Hkv;
+    const long long nw_o = effective_workers(tot_o, p.num_workers);
+    const long long a_o = (long long)Hkv * p.cum_own[b] + (long long)g * ob;
+    int wf_o = 0, n_o = 0;
+    if (ob > 0) {
+        wf_o = (int)(((a_o + 1) * nw_o - 1) / tot_o);
+        n_o = (int)(((a_o + ob) * nw_o - 1) / tot_o) - wf_o + 1;
+    }
+    if (sk == 0 && n_o == 1)
+        return;   // finished by a single worker
+    const long long tot_s = (long long)p.cum_shared[p.num_groups] * Hkv;
+    const long long nw_s = tot_s > 0 ? effective_workers(tot_s, p.num_workers) : 1;
+    long long a_s = 0;
+    int wf_s = 0, n_s = 0, row = 0;
+    if (sk > 0) {
+        a_s = (long long)Hkv * p.cum_shared[k] + (long long)g * sk;
+        wf_s = (int)(((a_s + 1) * nw_s - 1) / tot_s);
+        n_s = (int)(((a_s + sk) * nw_s - 1) / tot_s) - wf_s + 1;
+        row = (b - p.group_start[k]) * G + hl;
+    }
+    const int np = n_s + n_o;
+    // Piece i: lane-held code = shared (bit 31) | unit area (bit 30) | slot << 6 | row, or -1 if the
+    // worker's range is empty. Slots stay below 2^17 (workers) and unit indices below B Hkv < 2^24,
+    // so no code is -1.
+    const int lead = sk > 0 ? p.group_start[k] : 0;
+    auto piece = [&](int i) -> int {
+        if (i < n_s) {
+            if (n_s == 1)
+                return (int)(0xC0000000u | ((uint32_t)(lead * Hkv + g) << 6) | (uint32_t)row);
+            const long long w = wf_s + i;
+            const long long s = w * tot_s / nw_s;
+            if (s == (w + 1) * tot_s / nw_s)
+                return -1;
+            const long long slot = 2 * w + ((w == wf_s && s < a_s) ? 1 : 0);
+            return (int)(0x80000000u | (uint32_t)(slot << 6) | (uint32_t)row);
+        }
+        if (n_o == 1)   // sk > 0 here: a whole own unit of an unshared sequence was written out
+            return (int)(0x40000000u | ((uint32_t)(b * Hkv + g) << 6) | (uint32_t)hl);
+        const long long w = wf_o + (i - n_s);
+        const long long s = w * tot_o / nw_o;
+        if (s == (w + 1) * tot_o / nw_o)
+            return -1;
+        const long long slot = 2 * w + ((w == wf_o && s < a_o) ? 1 : 0);
+        return (int)((uint32_t)(slot << 6) | (uint32_t)hl);
+    };
+    auto ml_of = [&](int code) -> const float * {
+        const size_t slot = (size_t)((uint32_t)code & 0x3fffffffu) >> 6;
+        const size_t r = (size_t)(code & 63);
+        const bool unit = ((uint32_t)code & 0x40000000u) != 0;
+        if (code < 0)
+            return (unit ? p.shared_unit_ml : p.shared_ml) + (slot * kPrefixRows + r) * 2;
+        return (unit ? p.own_unit_ml : p.own_ml) + (slot * G + r) * 2;
+    };
+    auto acc_of = [&](int code) -> const float * {
+        const size_t slot = (size_t)((uint32_t)code & 0x3fffffffu) >> 6;
+        const size_t r = (size_t)(code & 63);
+        const bool unit = ((uint32_t)code & 0x40000000u) != 0;
+        if (code < 0)
+            return (unit ? p.shared_unit_acc : p.shared_acc) + (slot * kPrefixRows + r) * D;
+        return (unit ? p.own_unit_acc : p.own_acc) + (slot * G + r) * D;
+    };
+    float M = -__builtin_inff();
+    for (int c0 = 0; c0 < np; c0 += kWave) {
+        float m = -__builtin_inff();
+        if (c0 + lane < np) {
+            const int code = piece(c0 + lane);
+            if (code != -1)
+                m = ml_of(code)[0];
+        }
+        M = fmaxf(M, wave_max(m));
+    }
+    float Lsum = 0.0f;
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+        acc[e] = 0.0f;
+    for (int c0 = 0; c0 < np; c0 += kWave) {
+        float c = 0.0f, l = 0.0f;
+        int code = -1;
+        if (c0 + lane < np) {
+            code = piece(c0 + lane);
+            if (code != -1) {
+                const f32x2_t ml = *reinterpret_cast<const f32x2_t *>(ml_of(code));
+                c = __builtin_amdgcn_exp2f(ml[0] - M);
+                l = ml[1];
+            }
+        }
+        Lsum += wave_sum(c * l);
+        const int cnt = min(kWave, np - c0);
+        for (int i = 0; i < cnt; ++i) {
+            const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), i));
+            const int ki = __builtin_amdgcn_readlane(code, i);
+            if (ki == -1 || ci == 0.0f)
+                continue;
+            const float *src = acc_of(ki) + E * lane;
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                acc[e] += ci * src[e];
+        }
+    }
+    const float inv = bad ? __builtin_nanf("") : 1.0f / Lsum;
+    if constexpr (E == 2) {
+        const f32x2_t o = {acc[0] * inv, acc[1] * inv};
+        *reinterpret_cast<bf16x2_t *>(dst) = __builtin_convertvector(o, bf16x2_t);
+    } else {
+        *reinterpret_cast<__bf16 *>(dst) = (__bf16)(acc[0] * inv);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream)
@@ -149,6 +292,24 @@ hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream)
         hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(kMergeThreads), 0, stream, p);
     else if (head_dim == 64)
         hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(kMergeThreads), 0, stream, p);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace sl
+
+namespace sl {
+
+hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream)
+{
+    const long long items = (long long)p.batch * p.num_q_heads;
+    const int per_block = kMergeThreads / kWave;
+    const dim3 grid((unsigned)((items + per_block - 1) / per_block));
+    if (head_dim == 128)
+        hipLaunchKernelGGL(merge_prefix_kernel<128>, grid, dim3(kMergeThreads), 0, stream, p);
+    else if (head_dim == 64)
+        hipLaunchKernelGGL(merge_prefix_kernel<64>, grid, dim3(kMergeThreads), 0, stream, p);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

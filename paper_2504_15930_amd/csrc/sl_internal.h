@@ -68,6 +68,15 @@ struct TileEntry {
 constexpr uint32_t kMetaLast = 1u << 4;
 constexpr uint32_t kMetaFirst = 1u << 5;
 constexpr uint32_t kMetaBadLen = 1u << 6;
+constexpr uint32_t kMetaPrefixed = 1u << 7;   // own-page unit of a sequence whose first pages are shared
+// Prefix-sharing mode: a shared-prefix tile list holds, per (group, KV head),
+// the group's shared pages once; its entries keep members - 1 in bits [3:0]
+// (every shared page is full) and the first query row of the group's first
+// member in [31:8]. The query rows of a shared unit are (member j, head h) ->
+// row0 + j * Hq + h, at most kPrefixRows of them (kPrefixBlocks MFMA column
+// blocks of 16).
+constexpr int kPrefixBlocks = 4;
+constexpr int kPrefixRows = 16 * kPrefixBlocks;
 constexpr int kMetaRowShift = 8;
 
 struct Workspace {
@@ -97,7 +106,45 @@ struct SplitParams {
     float *part_ml;
     float *part_acc;
     int32_t batch, num_kv_heads, group, num_workers;
+    int32_t num_q_heads;   // query-row stride of one sequence (prefix mode)
     float scale_log2;      // scale * log2(e): scores are kept in base-2 units
+    // Prefix mode: a unit seen whole by one worker that still has to be merged
+    // (a shared unit, or the own pages of a sequence with shared pages) keeps
+    // its partial state here, at unit index (first query row) / G, with the
+    // row stride of part_ml / part_acc; null otherwise.
+    float *unit_ml;
+    float *unit_acc;
+};
+
+// Prefix-sharing mode. Groups are runs of consecutive sequences
+// [group_start[k], group_start[k+1]) whose first shared_pages[k] block-table
+// entries are the same; the group's first member's entries are used.
+struct PrefixPartitionParams {
+    const int32_t *seq_lens;
+    const int32_t *block_table;
+    const int32_t *group_start;   // [num_groups + 1]
+    const int32_t *shared_pages;  // [num_groups]
+    int32_t *cum_own;             // [B + 1] prefix sum of own (unshared) pages
+    int32_t *cum_shared;          // [num_groups + 1] prefix sum of shared pages
+    int32_t *seq_group;           // [B] group of each sequence, -1 if unshared
+    TileEntry *own_tiles;         // [B * max_blocks * Hkv]
+    TileEntry *shared_tiles;      // [num_groups * max_blocks * Hkv]
+    int32_t batch, num_groups, num_q_heads, num_kv_heads, max_blocks, num_pages;
+};
+
+struct PrefixMergeParams {
+    const int32_t *seq_lens;
+    const int32_t *group_start;
+    const int32_t *shared_pages;
+    const int32_t *cum_own;
+    const int32_t *cum_shared;
+    const int32_t *seq_group;
+    const float *own_ml, *own_acc;        // [2 NW][G][2], [2 NW][G][D]
+    const float *shared_ml, *shared_acc;  // [2 NW][kPrefixRows][2], [2 NW][kPrefixRows][D]
+    const float *own_unit_ml, *own_unit_acc;        // [B Hkv][G][2 | D]: whole own units
+    const float *shared_unit_ml, *shared_unit_acc;  // [B Hkv][kPrefixRows][2 | D]: whole shared units
+    uint16_t *out;
+    int32_t batch, num_groups, num_q_heads, num_kv_heads, group, num_workers, max_blocks;
 };
 
 struct MergeParams {
@@ -121,12 +168,28 @@ struct AppendParams {
     int32_t batch, num_kv_heads, max_blocks, num_pages;
 };
 
+constexpr int kMaxPrefixBatch = 4096;      // the prefix partitioner keeps three ints per sequence in LDS
+
+struct PrefixWorkspace {
+    int32_t *cum_own, *seq_group, *cum_shared;
+    TileEntry *own_tiles, *shared_tiles;
+    float *own_ml, *own_acc, *shared_ml, *shared_acc;
+    float *own_unit_ml, *own_unit_acc, *shared_unit_ml, *shared_unit_acc;
+};
+size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group, int head_dim,
+                               int num_workers, int num_groups, PrefixWorkspace *ws);
+
 // Layout of the workspace for the given sizes; `base` may be null to size it.
 size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
                         int head_dim, int num_workers, Workspace *ws);
 
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
+// Prefix mode: the shared pass (kPrefixBlocks column blocks per tile, partial
+// states only) and the partitioner / merge around the two passes.
+hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream);
+hipError_t launch_partition_prefix(const PrefixPartitionParams &p, hipStream_t stream);
+hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Decode engine helpers (engine.hip): apply a step's lengths and block-table

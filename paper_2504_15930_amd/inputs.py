@@ -237,6 +237,44 @@ def quantize_e4m3(x: torch.Tensor, live: torch.Tensor, chunk: int = 1 << 13):
     return codes, scales
 
 
+def make_grpo_batch(num_prompts: int, samples: int, prompt_len: int, *, seed: int = 0, device="cpu",
+                    num_q_heads: int = 28, num_kv_heads: int = 4, head_dim: int = 128,
+                    gen_median: float = 512.0, gen_sigma: float = 1.0, gen_cap: int = 4096,
+                    poison: bool = True):
+    """A GRPO-like decode batch: ``samples`` consecutive sequences per prompt share the prompt's
+    floor(prompt_len / 16) full pages (same page ids, hence the same tokens) and continue on
+    pages of their own; each has generated floor(X) tokens, ln X ~ N(ln gen_median, gen_sigma^2),
+    clipped to [0, gen_cap]. Returns (batch, group_start [num_prompts + 1], shared_pages
+    [num_prompts]) with the two int32 tensors on ``device``."""
+    rng = np.random.default_rng(seed)
+    B = num_prompts * samples
+    gen = np.clip(np.floor(np.exp(rng.normal(np.log(gen_median), gen_sigma, B))), 0, gen_cap).astype(np.int64)
+    lengths = prompt_len + gen
+    sp = prompt_len // PAGE_SIZE
+    own = -(-lengths // PAGE_SIZE) - sp
+    total = num_prompts * sp + int(own.sum())
+    perm = rng.permutation(total).astype(np.int32)
+    poison_page = total
+    max_blocks = max(1, int((-(-lengths // PAGE_SIZE)).max()))
+    table = np.full((B, max_blocks), poison_page, dtype=np.int32)
+    pos = 0
+    for k in range(num_prompts):
+        common = perm[pos:pos + sp]
+        pos += sp
+        for b in range(k * samples, (k + 1) * samples):
+            table[b, :sp] = common
+            table[b, sp:sp + own[b]] = perm[pos:pos + own[b]]
+            pos += own[b]
+    batch = make_paged_batch(lengths, num_q_heads, num_kv_heads, head_dim, seed=seed, device=device,
+                             block_table=table, num_pages=total + 1, rng=rng, poison=poison,
+                             meta=dict(workload="grpo", prompts=num_prompts, samples=samples, prompt_len=prompt_len))
+    batch.poison_page = poison_page
+    dev = torch.device(device)
+    starts = torch.arange(0, B + 1, samples, dtype=torch.int32, device=dev)
+    shared = torch.full((num_prompts,), sp, dtype=torch.int32, device=dev)
+    return batch, starts, shared
+
+
 def make_batch(name: str, seed: int = 0, device="cpu", poison: bool = True) -> Batch:
     """The named workload's decode step, drawn with ``seed``."""
     w = WORKLOADS[name]

@@ -19,7 +19,8 @@ SL_OK = 0
 STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_UNSUPPORTED",
                 -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
-           "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_status_string"]
+           "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_decode_attn_prefix",
+           "sl_decode_attn_prefix_workspace_size", "sl_status_string"]
 # include/sl_engine.h (typed in engine.py)
 ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
 # include/sl_dispatch.h (typed in dispatch.py)
@@ -72,6 +73,8 @@ def load(path: str = LIBRARY) -> ctypes.CDLL:
     lib.sl_decode_attn.argtypes = [D, P, P, P, P, P, ctypes.c_float, P]
     lib.sl_decode_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_float, P]
     lib.sl_kv_append.argtypes = [D, P, P, P, P, P, P]
+    lib.sl_decode_attn_prefix.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_float, P]
+    lib.sl_decode_attn_prefix_workspace_size.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
     lib.sl_kv_append_fp8.argtypes = [D, P, P, P, P, P, P, P, P]
     lib.sl_status_string.argtypes = [ctypes.c_int]
     lib.sl_status_string.restype = ctypes.c_char_p
@@ -267,3 +270,47 @@ def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, k_scales
                                   block_table.data_ptr(), seq_lens.data_ptr(), k_pages.data_ptr(),
                                   v_pages.data_ptr())
             _check(st, "sl_kv_append")
+
+
+def decode_attn_prefix(q, k_pages, v_pages, block_table, seq_lens, scale, group_start, shared_pages, *,
+                       out=None, num_workers=0, workspace=None, timing=None) -> torch.Tensor:
+    """``sl_decode_attn_prefix``: decode attention reading each group's shared pages once.
+
+    ``group_start`` (int32 [G+1]) and ``shared_pages`` (int32 [G]) are device tensors;
+    consecutive sequences of a group share their first ``shared_pages[k]`` pages.
+    """
+    _need(q, "q", torch.bfloat16, 3)
+    _need(k_pages, "k_pages", torch.bfloat16, 4)
+    _need(v_pages, "v_pages", torch.bfloat16, 4)
+    _need(block_table, "block_table", torch.int32, 2)
+    _need(seq_lens, "seq_lens", torch.int32, 1)
+    _need(group_start, "group_start", torch.int32, 1)
+    _need(shared_pages, "shared_pages", torch.int32, 1)
+    ng = shared_pages.shape[0]
+    if group_start.shape[0] != ng + 1:
+        raise ValueError("group_start must have num_groups + 1 entries")
+    B, Hq, D = q.shape
+    N, Hkv, P, D2 = k_pages.shape
+    if D2 != D or v_pages.shape != k_pages.shape or block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("shape mismatch")
+    if out is None:
+        out = torch.empty_like(q)
+    lib = load()
+    with torch.cuda.device(q.device):
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+        desc = make_desc(B, Hq, Hkv, D, P, block_table.shape[1], N, num_workers, stream)
+        if B == 0:
+            return out
+        need = ctypes.c_size_t(0)
+        _check(lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(desc), ng, ctypes.byref(need)),
+               "sl_decode_attn_prefix_workspace_size")
+        ws = workspace if workspace is not None else _workspace(q.device, need.value)
+        desc.workspace = ws.data_ptr()
+        desc.workspace_bytes = ws.numel() * ws.element_size()
+        if timing is not None:
+            desc.timing_start, desc.timing_stop = timing
+        _check(lib.sl_decode_attn_prefix(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+                                         block_table.data_ptr(), seq_lens.data_ptr(), group_start.data_ptr(),
+                                         shared_pages.data_ptr(), ng, float(scale), out.data_ptr()),
+               "sl_decode_attn_prefix")
+    return out

@@ -1,0 +1,147 @@
+"""GPU parity of prefix-shared decode attention (sl_decode_attn_prefix) against the oracle.
+
+Sharing pages changes how often a page is read, not the result: every output
+row must match the attention oracle (the same definition as sl_decode_attn) to
+the bf16 tolerance. Batches are GRPO-like: several samples of one prompt share
+the prompt's full pages and continue on pages of their own.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle_pins as pins
+import parity
+from paper_2504_15930_amd import inputs, sl
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def grpo_case(rng, members, prompts, gen_max, Hq, Hkv, D, extra=0, shared_override=None):
+    """Groups of `members[k]` sequences whose first floor(prompts[k] / 16) pages are the same
+    page ids (and tokens); each member continues with `gen` tokens on pages of its own; `extra`
+    unshared sequences follow."""
+    lengths, starts, shared = [], [0], []
+    for m, p in zip(members, prompts):
+        lengths += [p + int(g) for g in rng.integers(0, gen_max + 1, m)]
+        starts.append(starts[-1] + m)
+        shared.append(p // 16)
+    lengths += [int(x) for x in rng.integers(1, 300, extra)]
+    B = len(lengths)
+    mb = max(-(-L // 16) for L in lengths) + 1
+    N = B * mb + 8
+    perm = list(rng.permutation(N))
+    table = np.zeros((B, mb), np.int32)
+    for k, m in enumerate(members):
+        sp = shared[k]
+        common = [perm.pop() for _ in range(sp)]
+        for b in range(starts[k], starts[k] + m):
+            table[b, :sp] = common
+            for i in range(sp, mb):
+                table[b, i] = perm.pop()
+    for b in range(starts[-1], B):
+        for i in range(mb):
+            table[b, i] = perm.pop()
+    if shared_override is not None:
+        shared = shared_override
+    case, dense = pins.random_case(rng, B, Hq, Hkv, D, 16, lengths, table=table)
+    return case, np.array(starts, np.int32), np.array(shared, np.int32)
+
+
+def _bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def run_prefix(case, starts, shared, num_workers=0):
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    out = sl.decode_attn_prefix(_bf16(case["q"]), _bf16(case["k_pages"]), _bf16(case["v_pages"]),
+                                d(case["block_table"]), d(case["seq_lens"]), case["scale"], d(starts), d(shared),
+                                num_workers=num_workers)
+    torch.cuda.synchronize()
+    return out
+
+
+CASES = [
+    # members, prompt lengths, max generated, Hq, Hkv, D, extra unshared sequences
+    ([8, 8, 1, 9], [100, 512, 40, 17], 200, 28, 4, 128, 3),
+    ([16, 3, 2], [64, 160, 300], 50, 16, 4, 64, 0),
+    ([4, 4], [1000, 33], 0, 8, 8, 128, 2),          # nothing generated: some contexts are all shared
+    ([2], [16], 5, 64, 8, 128, 1),                   # G = 8, one shared page
+]
+
+
+@pytest.mark.parametrize("case_id", range(len(CASES)))
+@pytest.mark.parametrize("workers", [0, 1, 7, 1000])
+def test_prefix_matches_oracle(case_id, workers):
+    members, prompts, gen, Hq, Hkv, D, extra = CASES[case_id]
+    rng = np.random.default_rng(40 + case_id)
+    case, starts, shared = grpo_case(rng, members, prompts, gen, Hq, Hkv, D, extra)
+    out = run_prefix(case, starts, shared, workers)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, f"case {case_id} workers {workers}")
+
+
+def test_no_groups_is_plain_attention():
+    rng = np.random.default_rng(50)
+    case, _, _ = grpo_case(rng, [3], [70], 30, 28, 4, 128, extra=4)
+    out = run_prefix(case, np.zeros(1, np.int32), np.zeros(0, np.int32))
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "no groups")
+
+
+def test_oversized_and_zero_share_groups_stay_exact():
+    """A group with more members than fit the 64 query rows, and groups sharing no page, are
+    attended without sharing."""
+    rng = np.random.default_rng(51)
+    case, starts, shared = grpo_case(rng, [10, 3, 2], [48, 33, 5], 40, 28, 4, 128)   # 10 * 7 = 70 > 64 rows
+    out = run_prefix(case, starts, shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "oversized group")
+
+
+def test_member_shorter_than_shared_prefix_gets_nan():
+    """A group whose page count fits the block table but exceeds its members' lengths: NaN rows
+    for the members (an invalid request), exact rows for everyone else."""
+    rng = np.random.default_rng(52)
+    case, starts, shared = grpo_case(rng, [4, 2], [64, 32], 20, 28, 4, 128)
+    shared = shared.copy()
+    mb = case["block_table"].shape[1]               # one more than any sequence's page count
+    assert (case["seq_lens"][:4] < 16 * mb).all()
+    shared[0] = mb                                  # in bounds, but longer than every member
+    out = run_prefix(case, starts, shared).float().cpu().numpy()
+    assert np.isnan(out[:4]).all()
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(torch.from_numpy(out[4:]).to(torch.bfloat16), ref[4:], "other group")
+
+
+def test_full_size_grpo_batch():
+    """32 prompts x 8 samples, 7B-like heads, 1024-token prompts (64 shared pages), generated
+    lengths lognormal (median 512, capped at 4096): sampled rows against the oracle."""
+    b, starts, shared = inputs.make_grpo_batch(32, 8, 1024, seed=3, device=DEV)
+    torch.cuda.synchronize()
+    out = sl.decode_attn_prefix(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, starts, shared)
+    torch.cuda.synchronize()
+    rows = parity.sample_rows(b.seq_lens.cpu().numpy(), 24)
+    parity.assert_parity(out[rows], parity.oracle_rows(b, rows), "grpo")
+    plain = sl.run_batch(b)
+    torch.cuda.synchronize()
+    parity.assert_parity(out[rows], parity.oracle_rows(b, rows), "grpo")
+    assert (out.float() - plain.float()).abs().max().item() < 0.05
+
+
+def test_page_count_beyond_block_table_is_unshared():
+    """A shared page count larger than the block table's width is out of bounds: that group is
+    attended without sharing, exactly."""
+    rng = np.random.default_rng(53)
+    case, starts, shared = grpo_case(rng, [4, 3], [64, 40], 20, 28, 4, 128)
+    shared = shared.copy()
+    shared[0] = case["block_table"].shape[1] + 1
+    out = run_prefix(case, starts, shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "page count beyond the table")
