@@ -180,6 +180,67 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
     return res
 
 
+def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
+    """Prefix sharing on a GRPO-like batch with this workload's heads: 32 prompts x 8 samples,
+    1024-token prompts (64 shared pages per group), generated lengths lognormal (median 512,
+    sigma 1, capped at 4096). Plain decode attention reads every sample's copy of the prompt
+    pages; the prefix path reads each group's once. ``unique_bytes`` counts what the prefix path
+    has to read (shared pages once per group)."""
+    import torch
+
+    from paper_2504_15930_amd import inputs, sl
+
+    prompts, samples, prompt_len = 32, 8, 1024
+    b, starts, shared = inputs.make_grpo_batch(prompts, samples, prompt_len, seed=seed + 11, device=dev,
+                                               num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
+                                               head_dim=w.head_dim)
+    torch.cuda.synchronize()
+    L = b.seq_lens.cpu().numpy().astype(np.int64)
+    Hq, Hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+    plain_bytes = algorithmic_bytes(L, Hq, Hkv, D, 2)
+    sp = prompt_len // 16
+    own_tokens = int((L - 16 * sp).sum())
+    own_pages = int((-(-L // 16) - sp).sum())
+    unique_bytes = ((prompts * sp * 16 + own_tokens) * Hkv * 2 * D * 2 + len(L) * 2 * Hq * D * 2
+                    + (prompts * sp + own_pages) * 4)
+    out = torch.empty_like(b.q)
+
+    def plain():
+        sl.run_batch(b, out=out)
+
+    def prefixed():
+        sl.decode_attn_prefix(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, starts, shared,
+                              out=out)
+
+    res = {}
+    for name, fn in (("plain", plain), ("prefix", prefixed)):
+        for _ in range(warmup):
+            fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / steps
+    return {
+        "what": "decode attention with prefix sharing vs plain, GRPO-like batch",
+        "config": {"prompts": prompts, "samples": samples, "prompt_len": prompt_len, "gen_median": 512,
+                   "gen_sigma": 1.0, "gen_cap": 4096, "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D,
+                   "total_tokens": int(L.sum()), "max_seq_len": int(L.max())},
+        "plain_ms": round(res["plain"], 5),
+        "prefix_ms": round(res["prefix"], 5),
+        "speedup": round(res["plain"] / res["prefix"], 3),
+        "plain_bytes": plain_bytes,
+        "unique_bytes": unique_bytes,
+        "plain_GBps": round(plain_bytes / (res["plain"] * 1e-3) / 1e9, 2),
+        "prefix_unique_GBps": round(unique_bytes / (res["prefix"] * 1e-3) / 1e9, 2),
+        "prefix_effective_GBps": round(plain_bytes / (res["prefix"] * 1e-3) / 1e9, 2),
+    }
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
@@ -288,6 +349,8 @@ def main(argv=None) -> int:
                     help="also run a whole long-tail generation (decode engine, LPT vs FIFO admission); 0 skips it")
     ap.add_argument("--dispatch", type=int, default=1,
                     help="also run skewness-aware against random dispatching on the decode engine; 0 skips it")
+    ap.add_argument("--prefix", type=int, default=1,
+                    help="also time prefix-shared against plain decode attention on a GRPO-like batch; 0 skips it")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="instead of the benchmark, run `steps` plain device-to-device copies of "
                          "BYTES bytes (the reference kernel for scaling HBM counters)")
@@ -457,6 +520,9 @@ def main(argv=None) -> int:
         "GBps": round((nbytes + app_bytes) / (decode_ms * 1e-3) / 1e9, 2),
     }
 
+    if args.prefix and kvb == 2:
+        print("[bench] prefix sharing", file=sys.stderr, flush=True)
+        result["prefix"] = prefix_experiment(w, args.seed, dev, args.steps, args.warmup)
     if args.generation:
         result["generation"] = generation(w, batch.kv_dtype == "e4m3", args.seed, dev)
     if args.dispatch:

@@ -52,6 +52,11 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
+// A partial state l = sum 2^(s - m), acc = sum 2^(s - m) v is exact for any
+// reference m. Shared-prefix units raise m only when a score exceeds it by
+// more than this slack (base-2 units), which bounds the weights by 2^8 and
+// leaves the accumulators untouched on most tiles after a unit's first.
+constexpr float kRescaleSlack = 8.0f;
 #ifndef SL_NBUF
 #define SL_NBUF 2
 #endif
@@ -286,7 +291,7 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
                 sc[r] = kNegInf;
     }
     const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-    if (mx > st.m) {
+    if (mx > st.m + kRescaleSlack) {
         const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a unit's first tile
         st.l *= alpha;
 #pragma unroll
@@ -413,12 +418,23 @@ __device__ __forceinline__ void reset(PieceMulti<D, CB> &st)
     }
 }
 
+// Query rows of a shared-prefix unit staged in LDS: kPrefixRows rows of D
+// bf16, row r's 16-byte chunk j stored at chunk r * (D / 8) + (j ^ q_swizzle(r))
+// so that the 16 rows one block's lanes read at a time fall in distinct banks.
+template <int D>
+__device__ __forceinline__ int q_swizzle(int r)
+{
+    return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+
 // One tile of a shared-prefix unit (bf16 cache, every page full): the K and V
 // operands are formed once and feed the score and value MFMAs of all CB
 // column blocks, so each shared page is read once for all the group's rows.
+// The score MFMA's query operands of block cb are read from the LDS stage
+// `qs` when needed, which keeps the registers for the CB accumulators.
 template <int D, int CB>
 __device__ __forceinline__ void compute_tile_multi(PieceMulti<D, CB> &st, const Tile<D, false, CB> &t,
-                                                   const bf16x8_t (&qop)[CB][D / 32], float score_mul,
+                                                   const uint8_t *qs, float score_mul,
                                                    uint8_t *lds, int lane, int n, int quad)
 {
     u32x4_t kc[D / 32];
@@ -426,18 +442,21 @@ __device__ __forceinline__ void compute_tile_multi(PieceMulti<D, CB> &st, const 
     constexpr int RW = D / 32;   // bf16 dwords per value row
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
+        const int r = 16 * cb + n;
         f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s)
-            s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kc[s]), qop[cb][s], s4,
-                                                         0, 0, 0);
+        for (int s = 0; s < D / 32; ++s) {
+            const int j = 4 * s + quad;   // dims 32 s + 8 quad .. + 7, as q_index for bf16
+            const bf16x8_t qv = *reinterpret_cast<const bf16x8_t *>(qs + 16 * (r * (D / 8) + (j ^ q_swizzle<D>(r))));
+            s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kc[s]), qv, s4, 0, 0, 0);
+        }
         float sc[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
             sc[r] = s4[r] * score_mul;
         const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-        if (mx > st.m[cb]) {
-            const float alpha = __builtin_amdgcn_exp2f(st.m[cb] - mx);
+        if (mx > st.m[cb] + kRescaleSlack) {
+            const float alpha = __builtin_amdgcn_exp2f(st.m[cb] - mx);   // 0 on a unit's first tile
             st.l[cb] *= alpha;
 #pragma unroll
             for (int i = 0; i < D / 16; ++i)
@@ -519,6 +538,9 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
     // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
     __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    // Shared-prefix units: per-wave stage of the unit's query rows.
+    __shared__ __attribute__((aligned(16))) uint8_t q_stage[kWavesPerBlock][CB > 1 ? kPrefixRows * D * 2 : 16];
+    uint8_t *qs = q_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 
     // This worker's tile-list entries, read through a bounds-checked buffer
     // resource; an index past the range is clamped to the last tile.
@@ -564,7 +586,7 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
 
     std::conditional_t<CB == 1, Piece<D>, PieceMulti<D, CB>> st;
     reset(st);
-    bf16x8_t qop[CB][D / 32];   // score-MFMA B operands of the current unit (zero columns past its rows)
+    bf16x8_t qop[D / 32];   // score-MFMA B operands of the current unit (zero columns past its rows)
     bool started = false;   // the current unit's first tile is inside this range
     bool bad = false;
     int slot_sel = 0;
@@ -583,33 +605,37 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
                     if constexpr (CB == 1) {
 #pragma unroll
                         for (int s = 0; s < D / 32; ++s)
-                            qop[0][s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
+                            qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
                     } else {
                         // Shared-prefix unit: column c of block cb is row r = 16 cb + c, member
-                        // r / G and head r % G of the group; columns past its rows are zero.
-                        // Loaded here, once per unit, rather than carried by every tile.
+                        // r / G and head r % G of the group. Its query rows go to the LDS stage
+                        // once per unit, straight from memory (lane L of load k fills chunk
+                        // 64 k + L); rows past the unit's copy its first row, and their columns
+                        // are never written out. The full counter wait keeps the stage's
+                        // readiness on this path, instead of a wait on every tile.
                         const int rows = ((int)(meta & 15u) + 1) * G;
+                        const size_t row0 = meta >> kMetaRowShift;
+                        typedef __attribute__((address_space(3))) void lds_void_t;
+                        typedef __attribute__((address_space(1))) void global_void_t;
 #pragma unroll
-                        for (int cb = 0; cb < CB; ++cb) {
-                            const int r = 16 * cb + n;
-                            const size_t row = (size_t)(meta >> kMetaRowShift) +
-                                               (r < rows ? (size_t)(r / G) * p.num_q_heads + (size_t)(r % G) : 0);
-                            const uint8_t *qrow = reinterpret_cast<const uint8_t *>(p.q + row * D);
-#pragma unroll
-                            for (int s = 0; s < D / 32; ++s)
-                                qop[cb][s] = __builtin_bit_cast(
-                                    bf16x8_t, r < rows ? ld128(qrow + 2 * q_index<D, FP8>(s, quad))
-                                                       : u32x4_t{0u, 0u, 0u, 0u});
+                        for (int k = 0; k < kPrefixRows * D * 2 / 1024; ++k) {
+                            const int c = 64 * k + lane;
+                            const int r = c / (D / 8);
+                            const int j = (c % (D / 8)) ^ q_swizzle<D>(r);
+                            const size_t row = row0 + (r < rows ? (size_t)(r / G) * p.num_q_heads + (size_t)(r % G) : 0);
+                            __builtin_amdgcn_global_load_lds((global_void_t *)(p.q + row * D + 8 * j),
+                                                             (lds_void_t *)(qs + 1024 * k), 16, 0, 0);
                         }
+                        __builtin_amdgcn_s_waitcnt(0);
                     }
                 }
                 started |= (meta & kMetaFirst) != 0;
                 bad |= t.bad_page || (meta & kMetaBadLen) != 0;
                 if constexpr (CB == 1)
-                    compute_tile<D, FP8>(st, t, qop[0], p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
+                    compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
                                          quad);
                 else
-                    compute_tile_multi<D, CB>(st, t, qop, p.scale_log2, lds, lane, n, quad);
+                    compute_tile_multi<D, CB>(st, t, qs, p.scale_log2, lds, lane, n, quad);
                 if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
                     // A unit cut by this range leaves its piece in the worker's slot 2w + slot_sel.
                     // A whole unit is written out, unless it still has to be merged (shared pages,
