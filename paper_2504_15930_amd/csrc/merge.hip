@@ -39,10 +39,23 @@ __device__ __forceinline__ float wave_sum(float x)
     return x;
 }
 
+// floor(x / y) for 0 <= x < 2^53, 0 < y < 2^31: a double quotient corrected by
+// one step (64-bit integer division is a long software sequence on the GPU).
+__device__ __forceinline__ long long div_floor(long long x, long long y)
+{
+    long long q = (long long)((double)x / (double)y);
+    if (q * y > x)
+        --q;
+    else if ((q + 1) * y <= x)
+        ++q;
+    return q;
+}
+
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p)
 {
     constexpr int E = D / kWave;   // output columns per lane (1 or 2)
+    constexpr int kBatch = 8;      // pieces whose rows are fetched together with the weights
     const int Hkv = p.num_kv_heads;
     const int G = p.group;
     const int item = blockIdx.x * (kMergeThreads / kWave) +
@@ -55,78 +68,109 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p)
     const int g = u - b * Hkv;
     const int lane = threadIdx.x & (kWave - 1);
     uint16_t *dst = p.out + ((size_t)b * p.num_q_heads + (size_t)g * G + j) * D + E * lane;
+    // First round trip: the unit's place in the tile stream.
     const int cb = p.cum_pages[b];
     const int nb = p.cum_pages[b + 1] - cb;
+    const int len = p.seq_lens[b];
+    const long long total = (long long)p.cum_pages[p.batch] * Hkv;
 
     if (nb == 0) {
-        const uint16_t fill = p.seq_lens[b] < 0 ? 0x7fc0 : 0x0000;   // bf16 NaN / +0
+        const uint16_t fill = len < 0 ? 0x7fc0 : 0x0000;   // bf16 NaN / +0
 #pragma unroll
         for (int e = 0; e < E; ++e)
             dst[e] = fill;
         return;
     }
-    const long long total = (long long)p.cum_pages[p.batch] * Hkv;
     const long long NW = effective_workers(total, p.num_workers);
     const long long a = (long long)Hkv * cb + (long long)g * nb;   // first tile of the unit
     const long long e = a + nb;                                    // one past its last tile
     // Worker holding tile x: the largest w with floor(w * total / NW) <= x.
-    const int wf = (int)(((a + 1) * NW - 1) / total);
-    const int wl = (int)((e * NW - 1) / total);
+    const int wf = (int)div_floor((a + 1) * NW - 1, total);
+    const int wl = (int)div_floor(e * NW - 1, total);
     if (wf == wl)
         return;
+    const int np = wl - wf + 1;
 
-    // Pass 1: lane i owns piece wf + c0 + i. The slot of worker w is 2w, except
-    // for the unit's first worker when the unit began after that worker's
-    // first tile (then it was the worker's trailing piece, slot 2w + 1).
-    float M = -__builtin_inff();
-    for (int c0 = 0; c0 <= wl - wf; c0 += kWave) {
-        const int w = wf + c0 + lane;
-        float m = -__builtin_inff();
-        if (w <= wl) {
-            const long long s = (long long)w * total / NW;
-            if (s != (long long)(w + 1) * total / NW) {
-                const long long slot = 2LL * w + ((w == wf && s < a) ? 1 : 0);
-                m = p.part_ml[(slot * G + j) * 2];
+    // Piece i (lane i, i < 64) comes from worker wf + i. Its slot is 2w, except
+    // for the unit's first worker when the unit began after that worker's first
+    // tile (then it was the worker's trailing piece, slot 2w + 1). A worker with
+    // an empty range has no piece (slot -1).
+    auto slot_of = [&](int i) -> int {
+        const long long w = wf + i;
+        const long long s = div_floor(w * total, NW);
+        if (s == div_floor((w + 1) * total, NW))
+            return -1;
+        return (int)(2 * w + ((i == 0 && s < a) ? 1 : 0));
+    };
+    // Second round trip: the weights of up to 64 pieces and the rows of the
+    // first kBatch pieces, all loads issued together.
+    const int my_slot = lane < np ? slot_of(lane) : -1;
+    f32x2_t ml = {-__builtin_inff(), 0.0f};
+    if (my_slot >= 0)
+        ml = *reinterpret_cast<const f32x2_t *>(p.part_ml + ((size_t)my_slot * G + j) * 2);
+    float row[kBatch][E];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+        const int si = __builtin_amdgcn_readlane(my_slot, i);
+#pragma unroll
+        for (int k = 0; k < E; ++k)
+            row[i][k] = 0.0f;
+        if (i < np && si >= 0) {
+            const float *src = p.part_acc + ((size_t)si * G + j) * D + E * lane;
+            if constexpr (E == 2) {
+                const f32x2_t v = *reinterpret_cast<const f32x2_t *>(src);
+                row[i][0] = v[0];
+                row[i][1] = v[1];
+            } else {
+                row[i][0] = src[0];
             }
         }
-        M = fmaxf(M, wave_max(m));
     }
-    // Pass 2: weights per piece (in their lanes), then the weighted sums.
-    float Lsum = 0.0f;
+    float M = wave_max(ml[0]);
+    for (int c0 = kWave; c0 < np; c0 += kWave) {   // units spread over more than 64 workers
+        const int s2 = lane + c0 < np ? slot_of(lane + c0) : -1;
+        M = fmaxf(M, wave_max(s2 >= 0 ? p.part_ml[((size_t)s2 * G + j) * 2] : -__builtin_inff()));
+    }
+    // Weights c_i = 2^(m_i - M); a zero weight (empty worker, underflow) drops its row.
+    float c = my_slot >= 0 ? __builtin_amdgcn_exp2f(ml[0] - M) : 0.0f;
+    float Lsum = wave_sum(c * ml[1]);
     float acc[E];
 #pragma unroll
     for (int k = 0; k < E; ++k)
         acc[k] = 0.0f;
-    for (int c0 = 0; c0 <= wl - wf; c0 += kWave) {
-        const int w = wf + c0 + lane;
-        float c = 0.0f, l = 0.0f;
-        long long slot = 0;
-        if (w <= wl) {
-            const long long s = (long long)w * total / NW;
-            if (s != (long long)(w + 1) * total / NW) {
-                slot = 2LL * w + ((w == wf && s < a) ? 1 : 0);
-                const f32x2_t ml = *reinterpret_cast<const f32x2_t *>(p.part_ml + (slot * G + j) * 2);
-                c = __builtin_amdgcn_exp2f(ml[0] - M);
-                l = ml[1];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+        const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), i));
+#pragma unroll
+        for (int k = 0; k < E; ++k)
+            acc[k] += ci != 0.0f ? ci * row[i][k] : 0.0f;
+    }
+    // Pieces past the first kBatch (long units cut across many workers).
+    for (int c0 = 0; c0 < np; c0 += kWave) {
+        int sl = my_slot;
+        float cl = c;
+        if (c0 > 0) {
+            sl = lane + c0 < np ? slot_of(lane + c0) : -1;
+            float ml0 = -__builtin_inff(), ml1 = 0.0f;
+            if (sl >= 0) {
+                const f32x2_t v = *reinterpret_cast<const f32x2_t *>(p.part_ml + ((size_t)sl * G + j) * 2);
+                ml0 = v[0];
+                ml1 = v[1];
             }
+            cl = sl >= 0 ? __builtin_amdgcn_exp2f(ml0 - M) : 0.0f;
+            Lsum += wave_sum(cl * ml1);
         }
-        Lsum += wave_sum(c * l);
-        const int cnt = min(kWave, wl - wf - c0 + 1);
-        const int slot_lo = (int)slot;   // slots < 2^17, exchanged as 32-bit lanes
-#pragma unroll 4
-        for (int i = 0; i < cnt; ++i) {
-            const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), i));
-            const int si = __builtin_amdgcn_readlane(slot_lo, i);
-            if (ci == 0.0f)
-                continue;   // empty worker (or a weight that underflowed)
+        const int lo = c0 == 0 ? kBatch : 0;
+        const int cnt = min(kWave, np - c0);
+        for (int i = lo; i < cnt; ++i) {
+            const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cl), i));
+            const int si = __builtin_amdgcn_readlane(sl, i);
+            if (ci == 0.0f || si < 0)
+                continue;
             const float *src = p.part_acc + ((size_t)si * G + j) * D + E * lane;
-            if constexpr (E == 2) {
-                const f32x2_t v = *reinterpret_cast<const f32x2_t *>(src);
-                acc[0] += ci * v[0];
-                acc[1] += ci * v[1];
-            } else {
-                acc[0] += ci * src[0];
-            }
+#pragma unroll
+            for (int k = 0; k < E; ++k)
+                acc[k] += ci * src[k];
         }
     }
     const float inv = 1.0f / Lsum;
