@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIBRARY = os.path.join(HERE, "libsl.so")
-SOURCES = ["partition.hip", "decode_split.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
+SOURCES = ["partition.hip", "decode_split.hip", "decode_shared.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
            "engine.cpp", "dispatch.cpp"]
 ARCH = "gfx950"
 
@@ -22,6 +22,9 @@ HIPCC_FLAGS = [
     "-mcode-object-version=5",
     # no packed-fp32 instructions anywhere (the hardware forms are avoided on purpose)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the online softmax rescales them with
+    # vector ALU instructions, which cannot read accumulation registers
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -147,6 +147,11 @@ sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
     return SL_OK;
 }
 
+// Workgroups of the shared-page pass: each holds four wavefronts, so half
+// the single-unit worker count puts two such workgroups on a CU by default.
+// Never more than nw, for which the partial-state slots are sized.
+int shared_workers(int nw) { return nw / 2 > 0 ? nw / 2 : 1; }
+
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
@@ -346,7 +351,9 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.num_workers = nw;
     sp_.num_q_heads = d->num_q_heads;
     sp_.scale_log2 = scale * 1.4426950408889634f;
-    // shared pass
+    // shared pass: one workgroup of four wavefronts per worker
+    const int nws = shared_workers(nw);
+    sp_.num_workers = nws;
     sp_.tiles = ws.shared_tiles;
     sp_.cum_pages = ws.cum_shared;
     sp_.batch = num_groups;
@@ -359,6 +366,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     if (launch_split_shared(sp_, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     // own pass
+    sp_.num_workers = nw;
     sp_.tiles = ws.own_tiles;
     sp_.cum_pages = ws.cum_own;
     sp_.batch = d->batch;
@@ -393,6 +401,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     mp.num_kv_heads = d->num_kv_heads;
     mp.group = G;
     mp.num_workers = nw;
+    mp.num_shared_workers = nws;
     mp.max_blocks = d->max_blocks_per_seq;
     if (launch_merge_prefix(mp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;

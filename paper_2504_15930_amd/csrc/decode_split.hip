@@ -680,19 +680,6 @@ hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_
     return hipGetLastError();
 }
 
-hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream)
-{
-    const dim3 grid((p.num_workers + kWavesPerBlock - 1) / kWavesPerBlock);
-    const dim3 block(kWave * kWavesPerBlock);
-    if (head_dim == 128)
-        hipLaunchKernelGGL((split_kv_kernel<128, false, kPrefixBlocks>), grid, block, 0, stream, p);
-    else if (head_dim == 64)
-        hipLaunchKernelGGL((split_kv_kernel<64, false, kPrefixBlocks>), grid, block, 0, stream, p);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
-}
-
 hipError_t split_blocks_per_cu(int head_dim, bool fp8, int *blocks)
 {
     const int threads = kWave * kWavesPerBlock;

@@ -145,6 +145,7 @@ struct PrefixMergeParams {
     const float *shared_unit_ml, *shared_unit_acc;  // [B Hkv][kPrefixRows][2 | D]: whole shared units
     uint16_t *out;
     int32_t batch, num_groups, num_q_heads, num_kv_heads, group, num_workers, max_blocks;
+    int32_t num_shared_workers;   // workgroups of the shared-page pass
 };
 
 struct MergeParams {
