@@ -44,7 +44,7 @@ size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv
     };
     PrefixWorkspace w;
     w.cum_own = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
-    w.seq_group = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)batch));
+    w.seq_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4 * (size_t)batch));
     w.cum_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)num_groups + 1)));
     w.own_tiles = reinterpret_cast<TileEntry *>(take(sizeof(TileEntry) * (size_t)batch * max_blocks * num_kv_heads));
     w.shared_tiles =
@@ -327,7 +327,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     pp.shared_pages = sp;
     pp.cum_own = ws.cum_own;
     pp.cum_shared = ws.cum_shared;
-    pp.seq_group = ws.seq_group;
+    pp.seq_shared = ws.seq_shared;
     pp.own_tiles = ws.own_tiles;
     pp.shared_tiles = ws.shared_tiles;
     pp.batch = d->batch;
@@ -385,7 +385,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     mp.shared_pages = sp;
     mp.cum_own = ws.cum_own;
     mp.cum_shared = ws.cum_shared;
-    mp.seq_group = ws.seq_group;
+    mp.seq_shared = ws.seq_shared;
     mp.own_ml = ws.own_ml;
     mp.own_acc = ws.own_acc;
     mp.shared_ml = ws.shared_ml;

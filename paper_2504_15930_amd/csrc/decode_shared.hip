@@ -41,7 +41,7 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
-constexpr int kSharedWaves = kPrefixRows / 16;   // one wavefront per column block
+constexpr int kSharedWaves = kPrefixBlocks;   // one wavefront per 16-row column block
 constexpr int kAhead = 3;                        // tiles in flight beyond the one computed
 constexpr float kNegInf = -__builtin_inff();
 // A partial state l = sum 2^(s - m), acc = sum 2^(s - m) v is exact for any

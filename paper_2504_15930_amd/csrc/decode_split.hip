@@ -36,8 +36,6 @@
 // (v_cvt_scalef32_pk_bf16_fp8 with unit scale), the per-(page, head) key
 // scale multiplies the fp32 scores and the value scale multiplies the
 // probabilities before they are rounded for the value MFMA.
-#include <type_traits>
-
 #include "sl_internal.h"
 
 namespace sl {
@@ -53,7 +51,7 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
 // A partial state l = sum 2^(s - m), acc = sum 2^(s - m) v is exact for any
-// reference m. Shared-prefix units raise m only when a score exceeds it by
+// reference m. The running maximum is raised only when a score exceeds it by
 // more than this slack (base-2 units), which bounds the weights by 2^8 and
 // leaves the accumulators untouched on most tiles after a unit's first.
 constexpr float kRescaleSlack = 8.0f;
@@ -113,14 +111,14 @@ __device__ __forceinline__ float quad_sum(float x)
     return x + __shfl_xor(x, 32, kWave);
 }
 
-template <int D, bool FP8, int CB = 1>
+template <int D, bool FP8>
 struct Tile {
     // Per-lane dwords of K (score-MFMA A operands) and V (four rows).
     static constexpr int KW = FP8 ? D / 16 : D / 8;
     static constexpr int VW = FP8 ? D / 16 : D / 8;
     uint32_t k[KW];
     uint32_t v[VW];
-    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only (CB == 1)
+    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only
     float scl;           // FP8: key scale in lanes 0-31, value scale in lanes 32-63
     uint32_t meta;       // TileEntry::meta (wave-uniform)
     bool bad_page;       // the block table named a page outside the pool
@@ -134,8 +132,8 @@ __device__ __forceinline__ int q_index(int s, int quad)
 }
 
 // Issue every load of one tile. All loads are unconditional.
-template <int D, bool FP8, int CB = 1>
-__device__ __forceinline__ void issue_tile(Tile<D, FP8, CB> &t, const SplitParams &p, int32_t page,
+template <int D, bool FP8>
+__device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p, int32_t page,
                                            uint32_t meta, bool with_q, int n, int quad, int lane)
 {
     constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
@@ -189,13 +187,10 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8, CB> &t, const SplitParam
     // when the operand is formed.
     if (with_q) {
         const int G = p.group;
-        if constexpr (CB == 1) {
-            const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
+        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
 #pragma unroll
-            for (int s = 0; s < D / 32; ++s)
-                t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
-        }
-        // (shared-prefix units load their CB query blocks when the unit starts)
+        for (int s = 0; s < D / 32; ++s)
+            t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
     }
 }
 
@@ -205,15 +200,15 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8, CB> &t, const SplitParam
 // starting at quad D/64. A chunk c of row r is stored at position
 // c ^ ((r / P) % C) of its row (P rows per 256 bytes, C chunks per row), which
 // makes the 16-lane groups of both the writes and the reads hit distinct banks.
-template <int D, bool FP8, int CB>
-__device__ __forceinline__ void regroup_k(const Tile<D, FP8, CB> &t, uint8_t *lds, int lane, int n, int quad,
+template <int D, bool FP8>
+__device__ __forceinline__ void regroup_k(const Tile<D, FP8> &t, uint8_t *lds, int lane, int n, int quad,
                                           u32x4_t (&kc)[FP8 ? D / 64 : D / 32])
 {
     constexpr int R = D * (FP8 ? 1 : 2);   // bytes per row
     constexpr int C = R / 16;               // 16-byte chunks per row
     constexpr int P = 256 / R;              // rows per 256 bytes
 #pragma unroll
-    for (int i = 0; i < Tile<D, FP8, CB>::KW / 4; ++i) {
+    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
         const int off = 1024 * i + 16 * lane;
         const int r = off / R, c = (off % R) / 16;
         *reinterpret_cast<u32x4_t *>(lds + r * R + 16 * (c ^ ((r / P) % C))) =
@@ -268,7 +263,7 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
                                              int valid, uint8_t *lds, int lane, int n, int quad)
 {
     u32x4_t kc[FP8 ? D / 64 : D / 32];
-    regroup_k<D, FP8, 1>(t, lds, lane, n, quad, kc);
+    regroup_k<D, FP8>(t, lds, lane, n, quad, kc);
     f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
@@ -396,127 +391,7 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
     }
 }
 
-// ---- shared-prefix units: CB blocks of 16 query rows per tile ------------------
-
-template <int D, int CB>
-struct PieceMulti {
-    f32x4_t acc[CB][D / 16];
-    float m[CB];
-    float l[CB];
-};
-
-template <int D, int CB>
-__device__ __forceinline__ void reset(PieceMulti<D, CB> &st)
-{
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-#pragma unroll
-        for (int i = 0; i < D / 16; ++i)
-            st.acc[cb][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        st.m[cb] = kNegInf;
-        st.l[cb] = 0.f;
-    }
-}
-
-// Query rows of a shared-prefix unit staged in LDS: kPrefixRows rows of D
-// bf16, row r's 16-byte chunk j stored at chunk r * (D / 8) + (j ^ q_swizzle(r))
-// so that the 16 rows one block's lanes read at a time fall in distinct banks.
-template <int D>
-__device__ __forceinline__ int q_swizzle(int r)
-{
-    return D == 128 ? (r & 15) : ((r >> 1) & 7);
-}
-
-// One tile of a shared-prefix unit (bf16 cache, every page full): the K and V
-// operands are formed once and feed the score and value MFMAs of all CB
-// column blocks, so each shared page is read once for all the group's rows.
-// The score MFMA's query operands of block cb are read from the LDS stage
-// `qs` when needed, which keeps the registers for the CB accumulators.
-template <int D, int CB>
-__device__ __forceinline__ void compute_tile_multi(PieceMulti<D, CB> &st, const Tile<D, false, CB> &t,
-                                                   const uint8_t *qs, float score_mul,
-                                                   uint8_t *lds, int lane, int n, int quad)
-{
-    u32x4_t kc[D / 32];
-    regroup_k<D, false, CB>(t, lds, lane, n, quad, kc);
-    constexpr int RW = D / 32;   // bf16 dwords per value row
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-        const int r = 16 * cb + n;
-        f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-            const int j = 4 * s + quad;   // dims 32 s + 8 quad .. + 7, as q_index for bf16
-            const bf16x8_t qv = *reinterpret_cast<const bf16x8_t *>(qs + 16 * (r * (D / 8) + (j ^ q_swizzle<D>(r))));
-            s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kc[s]), qv, s4, 0, 0, 0);
-        }
-        float sc[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            sc[r] = s4[r] * score_mul;
-        const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-        if (mx > st.m[cb] + kRescaleSlack) {
-            const float alpha = __builtin_amdgcn_exp2f(st.m[cb] - mx);   // 0 on a unit's first tile
-            st.l[cb] *= alpha;
-#pragma unroll
-            for (int i = 0; i < D / 16; ++i)
-                st.acc[cb][i] *= alpha;
-            st.m[cb] = mx;
-        }
-        float pr[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m[cb]);
-        const uint32_t p01 = pack_bf16(pr[0], pr[1]);
-        const uint32_t p23 = pack_bf16(pr[2], pr[3]);
-        st.l[cb] += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
-        const i16x4_t pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
-#pragma unroll
-        for (int i = 0; i < D / 16; ++i) {
-            const int w = i >> 1;
-            uint32_t lo, hi;
-            if ((i & 1) == 0) {
-                lo = (t.v[0 * RW + w] & 0xffffu) | (t.v[1 * RW + w] << 16);
-                hi = (t.v[2 * RW + w] & 0xffffu) | (t.v[3 * RW + w] << 16);
-            } else {
-                lo = (t.v[0 * RW + w] >> 16) | (t.v[1 * RW + w] & 0xffff0000u);
-                hi = (t.v[2 * RW + w] >> 16) | (t.v[3 * RW + w] & 0xffff0000u);
-            }
-            const i16x4_t va = __builtin_bit_cast(i16x4_t, u32x2_t{lo, hi});
-            st.acc[cb][i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, st.acc[cb][i], 0, 0, 0);
-        }
-    }
-}
-
-// A shared-prefix unit always leaves partial states (each member still has
-// its own pages to merge): rows r < members * G of slot `slot` of
-// (part_ml, part_acc), kPrefixRows rows per slot.
-template <int D, int CB>
-__device__ __forceinline__ void finish_shared(PieceMulti<D, CB> &st, int rows, bool bad, float *part_ml,
-                                              float *part_acc, size_t slot, int n, int quad)
-{
-    const float poison = bad ? __builtin_nanf("") : 0.0f;
-    const int d0 = quad * (D / 4);
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-        const float l = quad_sum(st.l[cb]);
-        const int r = 16 * cb + n;
-        if (r >= rows)
-            continue;
-        float *dst = part_acc + (slot * kPrefixRows + r) * D + d0;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-            for (int i = 0; i < D / 16; i += 4)
-                *reinterpret_cast<f32x4_t *>(dst + q4 * (D / 16) + i) =
-                    f32x4_t{st.acc[cb][i][q4], st.acc[cb][i + 1][q4], st.acc[cb][i + 2][q4],
-                            st.acc[cb][i + 3][q4]} + poison;
-        if (quad == 0)
-            *reinterpret_cast<f32x2_t *>(part_ml + (slot * kPrefixRows + r) * 2) = f32x2_t{st.m[cb] + poison, l};
-    }
-}
-
-template <int D, bool FP8, int CB = 1>
+template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
     const int w = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -538,9 +413,6 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
     // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
     __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
-    // Shared-prefix units: per-wave stage of the unit's query rows.
-    __shared__ __attribute__((aligned(16))) uint8_t q_stage[kWavesPerBlock][CB > 1 ? kPrefixRows * D * 2 : 16];
-    uint8_t *qs = q_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 
     // This worker's tile-list entries, read through a bounds-checked buffer
     // resource; an index past the range is clamped to the last tile.
@@ -578,13 +450,13 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
         first_meta[k] = meta_of(first[k]);
     }
 
-    Tile<D, FP8, CB> buf[kNbuf];
+    Tile<D, FP8> buf[kNbuf];
 #pragma unroll
     for (int k = 0; k < kNbuf - 1; ++k)
-        issue_tile<D, FP8, CB>(buf[k], p, first_page[k], first_meta[k],
+        issue_tile<D, FP8>(buf[k], p, first_page[k], first_meta[k],
                            k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane);
 
-    std::conditional_t<CB == 1, Piece<D>, PieceMulti<D, CB>> st;
+    Piece<D> st;
     reset(st);
     bf16x8_t qop[D / 32];   // score-MFMA B operands of the current unit (zero columns past its rows)
     bool started = false;   // the current unit's first tile is inside this range
@@ -595,47 +467,20 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
         for (int k = 0; k < kNbuf; ++k) {
             const int i = i0 + k;
             const uint32_t next_meta = meta_of(ring[k]);
-            issue_tile<D, FP8, CB>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
+            issue_tile<D, FP8>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
                                (next_meta & kMetaFirst) != 0, n, quad, lane);
             ring[k] = entry(i + 2 * kNbuf - 1);
             if (i < ntiles) {
-                const Tile<D, FP8, CB> &t = buf[k];
+                const Tile<D, FP8> &t = buf[k];
                 const uint32_t meta = t.meta;
                 if (i == 0 || (meta & kMetaFirst) != 0) {
-                    if constexpr (CB == 1) {
 #pragma unroll
-                        for (int s = 0; s < D / 32; ++s)
-                            qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
-                    } else {
-                        // Shared-prefix unit: column c of block cb is row r = 16 cb + c, member
-                        // r / G and head r % G of the group. Its query rows go to the LDS stage
-                        // once per unit, straight from memory (lane L of load k fills chunk
-                        // 64 k + L); rows past the unit's copy its first row, and their columns
-                        // are never written out. The full counter wait keeps the stage's
-                        // readiness on this path, instead of a wait on every tile.
-                        const int rows = ((int)(meta & 15u) + 1) * G;
-                        const size_t row0 = meta >> kMetaRowShift;
-                        typedef __attribute__((address_space(3))) void lds_void_t;
-                        typedef __attribute__((address_space(1))) void global_void_t;
-#pragma unroll
-                        for (int k = 0; k < kPrefixRows * D * 2 / 1024; ++k) {
-                            const int c = 64 * k + lane;
-                            const int r = c / (D / 8);
-                            const int j = (c % (D / 8)) ^ q_swizzle<D>(r);
-                            const size_t row = row0 + (r < rows ? (size_t)(r / G) * p.num_q_heads + (size_t)(r % G) : 0);
-                            __builtin_amdgcn_global_load_lds((global_void_t *)(p.q + row * D + 8 * j),
-                                                             (lds_void_t *)(qs + 1024 * k), 16, 0, 0);
-                        }
-                        __builtin_amdgcn_s_waitcnt(0);
-                    }
+                    for (int s = 0; s < D / 32; ++s)
+                        qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
                 }
                 started |= (meta & kMetaFirst) != 0;
                 bad |= t.bad_page || (meta & kMetaBadLen) != 0;
-                if constexpr (CB == 1)
-                    compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n,
-                                         quad);
-                else
-                    compute_tile_multi<D, CB>(st, t, qs, p.scale_log2, lds, lane, n, quad);
+                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n, quad);
                 if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
                     // A unit cut by this range leaves its piece in the worker's slot 2w + slot_sel.
                     // A whole unit is written out, unless it still has to be merged (shared pages,
@@ -643,14 +488,11 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitP
                     // own slot in the unit area, indexed by (first query row) / G.
                     const uint32_t row0 = meta >> kMetaRowShift;
                     const bool whole = started && (meta & kMetaLast) != 0;
-                    const bool to_unit = whole && (CB > 1 || (meta & kMetaPrefixed) != 0);
+                    const bool to_unit = whole && (meta & kMetaPrefixed) != 0;
                     float *const pml = to_unit ? p.unit_ml : p.part_ml;
                     float *const pacc = to_unit ? p.unit_acc : p.part_acc;
                     const size_t slot = to_unit ? (size_t)(row0 / (uint32_t)G) : 2 * (size_t)w + slot_sel;
-                    if constexpr (CB == 1)
-                        finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
-                    else
-                        finish_shared<D, CB>(st, ((int)(meta & 15u) + 1) * G, bad, pml, pacc, slot, n, quad);
+                    finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
                     reset(st);
                     started = false;
                     bad = false;

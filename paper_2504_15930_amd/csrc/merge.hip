@@ -194,6 +194,7 @@ template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMergeParams p)
 {
     constexpr int E = D / kWave;
+    constexpr int kBatch = 8;   // pieces whose rows are fetched together with the weights
     const int Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
     const int item = blockIdx.x * (kMergeThreads / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (item >= p.batch * Hq)
@@ -204,10 +205,14 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
     const int hl = h - g * G;
     const int lane = threadIdx.x & (kWave - 1);
     uint16_t *dst = p.out + ((size_t)b * Hq + h) * D + E * lane;
+    // First round trip: the sequence's place in both tile streams.
+    const int32_t *info = p.seq_shared + 4 * (size_t)b;   // shared-page start, count, lead, group
+    const int s_start = info[0], sk = info[1], lead = info[2];
     const int L = p.seq_lens[b];
-    const int k = p.seq_group[b];
-    const int sk = k >= 0 ? p.cum_shared[k + 1] - p.cum_shared[k] : 0;
-    const int ob = p.cum_own[b + 1] - p.cum_own[b];
+    const int co = p.cum_own[b];
+    const int ob = p.cum_own[b + 1] - co;
+    const long long tot_o = (long long)p.cum_own[p.batch] * Hkv;
+    const long long tot_s = (long long)p.cum_shared[p.num_groups] * Hkv;
     const bool bad = L < 0 || L > p.max_blocks * kPageSize || L < sk * kPageSize;
     if (sk == 0 && ob == 0) {
         const uint16_t fill = L < 0 ? 0x7fc0 : 0x0000;   // bf16 NaN / +0
@@ -216,38 +221,35 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
             dst[e] = fill;
         return;
     }
-    const long long tot_o = (long long)p.cum_own[p.batch] * Hkv;
     const long long nw_o = effective_workers(tot_o, p.num_workers);
-    const long long a_o = (long long)Hkv * p.cum_own[b] + (long long)g * ob;
+    const long long a_o = (long long)Hkv * co + (long long)g * ob;
     int wf_o = 0, n_o = 0;
     if (ob > 0) {
-        wf_o = (int)(((a_o + 1) * nw_o - 1) / tot_o);
-        n_o = (int)(((a_o + ob) * nw_o - 1) / tot_o) - wf_o + 1;
+        wf_o = (int)div_floor((a_o + 1) * nw_o - 1, tot_o);
+        n_o = (int)div_floor((a_o + ob) * nw_o - 1, tot_o) - wf_o + 1;
     }
     if (sk == 0 && n_o == 1)
         return;   // finished by a single worker
-    const long long tot_s = (long long)p.cum_shared[p.num_groups] * Hkv;
     const long long nw_s = tot_s > 0 ? effective_workers(tot_s, p.num_shared_workers) : 1;
     long long a_s = 0;
     int wf_s = 0, n_s = 0, row = 0;
     if (sk > 0) {
-        a_s = (long long)Hkv * p.cum_shared[k] + (long long)g * sk;
-        wf_s = (int)(((a_s + 1) * nw_s - 1) / tot_s);
-        n_s = (int)(((a_s + sk) * nw_s - 1) / tot_s) - wf_s + 1;
-        row = (b - p.group_start[k]) * G + hl;
+        a_s = (long long)Hkv * s_start + (long long)g * sk;
+        wf_s = (int)div_floor((a_s + 1) * nw_s - 1, tot_s);
+        n_s = (int)div_floor((a_s + sk) * nw_s - 1, tot_s) - wf_s + 1;
+        row = (b - lead) * G + hl;
     }
     const int np = n_s + n_o;
-    // Piece i: lane-held code = shared (bit 31) | unit area (bit 30) | slot << 6 | row, or -1 if the
-    // worker's range is empty. Slots stay below 2^17 (workers) and unit indices below B Hkv < 2^24,
-    // so no code is -1.
-    const int lead = sk > 0 ? p.group_start[k] : 0;
+    // Piece i: code = shared (bit 31) | unit area (bit 30) | slot << 6 | row, or -1 if
+    // the worker's range is empty. Slots stay below 2^17 (workers) and unit indices
+    // below B Hkv < 2^24, so no code is -1.
     auto piece = [&](int i) -> int {
         if (i < n_s) {
             if (n_s == 1)
                 return (int)(0xC0000000u | ((uint32_t)(lead * Hkv + g) << 6) | (uint32_t)row);
             const long long w = wf_s + i;
-            const long long s = w * tot_s / nw_s;
-            if (s == (w + 1) * tot_s / nw_s)
+            const long long s = div_floor(w * tot_s, nw_s);
+            if (s == div_floor((w + 1) * tot_s, nw_s))
                 return -1;
             const long long slot = 2 * w + ((w == wf_s && s < a_s) ? 1 : 0);
             return (int)(0x80000000u | (uint32_t)(slot << 6) | (uint32_t)row);
@@ -255,8 +257,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
         if (n_o == 1)   // sk > 0 here: a whole own unit of an unshared sequence was written out
             return (int)(0x40000000u | ((uint32_t)(b * Hkv + g) << 6) | (uint32_t)hl);
         const long long w = wf_o + (i - n_s);
-        const long long s = w * tot_o / nw_o;
-        if (s == (w + 1) * tot_o / nw_o)
+        const long long s = div_floor(w * tot_o, nw_o);
+        if (s == div_floor((w + 1) * tot_o, nw_o))
             return -1;
         const long long slot = 2 * w + ((w == wf_o && s < a_o) ? 1 : 0);
         return (int)((uint32_t)(slot << 6) | (uint32_t)hl);
@@ -277,37 +279,65 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
             return (unit ? p.shared_unit_acc : p.shared_acc) + (slot * kPrefixRows + r) * D;
         return (unit ? p.own_unit_acc : p.own_acc) + (slot * G + r) * D;
     };
-    float M = -__builtin_inff();
-    for (int c0 = 0; c0 < np; c0 += kWave) {
-        float m = -__builtin_inff();
-        if (c0 + lane < np) {
-            const int code = piece(c0 + lane);
-            if (code != -1)
-                m = ml_of(code)[0];
+    // Second round trip: the weights of up to 64 pieces and the rows of the
+    // first kBatch pieces, all loads issued together.
+    const int my_code = lane < np ? piece(lane) : -1;
+    f32x2_t ml = {-__builtin_inff(), 0.0f};
+    if (my_code != -1)
+        ml = *reinterpret_cast<const f32x2_t *>(ml_of(my_code));
+    float rowv[kBatch][E];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+        const int ci = __builtin_amdgcn_readlane(my_code, i);
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            rowv[i][e] = 0.0f;
+        if (i < np && ci != -1) {
+            const float *src = acc_of(ci) + E * lane;
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                rowv[i][e] = src[e];
         }
-        M = fmaxf(M, wave_max(m));
     }
-    float Lsum = 0.0f;
+    float M = wave_max(ml[0]);
+    for (int c0 = kWave; c0 < np; c0 += kWave) {   // more than 64 pieces
+        const int c2 = lane + c0 < np ? piece(lane + c0) : -1;
+        M = fmaxf(M, wave_max(c2 != -1 ? ml_of(c2)[0] : -__builtin_inff()));
+    }
+    // Weights c_i = 2^(m_i - M); a zero weight (empty worker, underflow) drops its row.
+    const float c = my_code != -1 ? __builtin_amdgcn_exp2f(ml[0] - M) : 0.0f;
+    float Lsum = wave_sum(c * ml[1]);
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e)
         acc[e] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+        const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), i));
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            acc[e] += ci != 0.0f ? ci * rowv[i][e] : 0.0f;
+    }
+    // Pieces past the first kBatch.
     for (int c0 = 0; c0 < np; c0 += kWave) {
-        float c = 0.0f, l = 0.0f;
-        int code = -1;
-        if (c0 + lane < np) {
-            code = piece(c0 + lane);
-            if (code != -1) {
-                const f32x2_t ml = *reinterpret_cast<const f32x2_t *>(ml_of(code));
-                c = __builtin_amdgcn_exp2f(ml[0] - M);
-                l = ml[1];
+        int cl = my_code;
+        float wl = c;
+        if (c0 > 0) {
+            cl = lane + c0 < np ? piece(lane + c0) : -1;
+            float m0 = -__builtin_inff(), l0 = 0.0f;
+            if (cl != -1) {
+                const f32x2_t v = *reinterpret_cast<const f32x2_t *>(ml_of(cl));
+                m0 = v[0];
+                l0 = v[1];
             }
+            wl = cl != -1 ? __builtin_amdgcn_exp2f(m0 - M) : 0.0f;
+            Lsum += wave_sum(wl * l0);
         }
-        Lsum += wave_sum(c * l);
+        const int lo = c0 == 0 ? kBatch : 0;
         const int cnt = min(kWave, np - c0);
-        for (int i = 0; i < cnt; ++i) {
-            const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c), i));
-            const int ki = __builtin_amdgcn_readlane(code, i);
+        for (int i = lo; i < cnt; ++i) {
+            const float ci = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wl), i));
+            const int ki = __builtin_amdgcn_readlane(cl, i);
             if (ki == -1 || ci == 0.0f)
                 continue;
             const float *src = acc_of(ki) + E * lane;

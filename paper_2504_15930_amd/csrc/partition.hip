@@ -250,8 +250,12 @@ __global__ __launch_bounds__(kPartitionThreads) void partition_prefix_kernel(Pre
             p.cum_own[i] = s_own[i];
         for (int i = tid; i <= NG; i += kPartitionThreads)
             p.cum_shared[i] = s_sh[i];
-        for (int i = tid; i < B; i += kPartitionThreads)
-            p.seq_group[i] = s_group[i];
+        for (int i = tid; i < B; i += kPartitionThreads) {
+            const int k = s_group[i];
+            typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+            *reinterpret_cast<i32x4_t *>(p.seq_shared + 4 * (size_t)i) =
+                k >= 0 ? i32x4_t{s_sh[k], s_sh[k + 1] - s_sh[k], p.group_start[k], k} : i32x4_t{0, 0, 0, -1};
+        }
     }
 
     const int Hkv = p.num_kv_heads;

@@ -126,7 +126,8 @@ struct PrefixPartitionParams {
     const int32_t *shared_pages;  // [num_groups]
     int32_t *cum_own;             // [B + 1] prefix sum of own (unshared) pages
     int32_t *cum_shared;          // [num_groups + 1] prefix sum of shared pages
-    int32_t *seq_group;           // [B] group of each sequence, -1 if unshared
+    int32_t *seq_shared;          // [B][4] per sequence: first shared page of its group in the shared
+                                  // stream, shared pages, group's first member, group (-1, zeros if unshared)
     TileEntry *own_tiles;         // [B * max_blocks * Hkv]
     TileEntry *shared_tiles;      // [num_groups * max_blocks * Hkv]
     int32_t batch, num_groups, num_q_heads, num_kv_heads, max_blocks, num_pages;
@@ -138,7 +139,7 @@ struct PrefixMergeParams {
     const int32_t *shared_pages;
     const int32_t *cum_own;
     const int32_t *cum_shared;
-    const int32_t *seq_group;
+    const int32_t *seq_shared;   // [B][4], as written by the partitioner
     const float *own_ml, *own_acc;        // [2 NW][G][2], [2 NW][G][D]
     const float *shared_ml, *shared_acc;  // [2 NW][kPrefixRows][2], [2 NW][kPrefixRows][D]
     const float *own_unit_ml, *own_unit_acc;        // [B Hkv][G][2 | D]: whole own units
@@ -172,7 +173,7 @@ struct AppendParams {
 constexpr int kMaxPrefixBatch = 4096;      // the prefix partitioner keeps three ints per sequence in LDS
 
 struct PrefixWorkspace {
-    int32_t *cum_own, *seq_group, *cum_shared;
+    int32_t *cum_own, *seq_shared, *cum_shared;
     TileEntry *own_tiles, *shared_tiles;
     float *own_ml, *own_acc, *shared_ml, *shared_acc;
     float *own_unit_ml, *own_unit_acc, *shared_unit_ml, *shared_unit_acc;
@@ -186,8 +187,9 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
 
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
-// Prefix mode: the shared pass (kPrefixBlocks column blocks per tile, partial
-// states only) and the partitioner / merge around the two passes.
+// Prefix mode: the shared pass (one workgroup of kPrefixBlocks wavefronts per
+// worker, one 16-row column block each; partial states only; p.num_workers
+// counts workgroups) and the partitioner / merge around the two passes.
 hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_partition_prefix(const PrefixPartitionParams &p, hipStream_t stream);
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
