@@ -34,7 +34,8 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PEAK_HBM_GBS = 8000.0
 METRIC = "decode-attn achieved HBM GB/s (% of MI355X peak) + decode steps/s, long-tail batch"
-KERNEL_SOURCES = ["paper_2504_15930_amd/csrc/decode_split.hip", "paper_2504_15930_amd/csrc/sl_internal.h"]
+KERNEL_SOURCES = ["paper_2504_15930_amd/csrc/decode_split.hip", "paper_2504_15930_amd/csrc/decode_unit.h",
+                  "paper_2504_15930_amd/csrc/sl_internal.h"]
 
 
 def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int, head_dim: int,

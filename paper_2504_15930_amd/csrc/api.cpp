@@ -147,10 +147,13 @@ sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
     return SL_OK;
 }
 
-// Workgroups of the shared-page pass: each holds four wavefronts, so half
-// the single-unit worker count puts two such workgroups on a CU by default.
-// Never more than nw, for which the partial-state slots are sized.
-int shared_workers(int nw) { return nw / 2 > 0 ? nw / 2 : 1; }
+// Workgroups of the shared-page pass. They run in the same launch as the
+// own-page workers (four per workgroup, nw / 4 workgroups): one shared-page
+// workgroup per own-page workgroup puts one of each on every CU by default,
+// the best ratio measured on MI355X (an eighth or three eighths of nw were
+// both about 12% slower). Never more than nw, for which the partial-state
+// slots are sized.
+int shared_workers(int nw) { return nw / 4 > 0 ? nw / 4 : 1; }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -351,21 +354,18 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.num_workers = nw;
     sp_.num_q_heads = d->num_q_heads;
     sp_.scale_log2 = scale * 1.4426950408889634f;
-    // shared pass: one workgroup of four wavefronts per worker
+    // Shared-page pass: one workgroup of four wavefronts per worker.
     const int nws = shared_workers(nw);
-    sp_.num_workers = nws;
-    sp_.tiles = ws.shared_tiles;
-    sp_.cum_pages = ws.cum_shared;
-    sp_.batch = num_groups;
-    sp_.part_ml = ws.shared_ml;
-    sp_.part_acc = ws.shared_acc;
-    sp_.unit_ml = ws.shared_unit_ml;
-    sp_.unit_acc = ws.shared_unit_acc;
-    if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
-        return SL_ERR_HIP;
-    if (launch_split_shared(sp_, d->head_dim, d->stream) != hipSuccess)
-        return SL_ERR_HIP;
-    // own pass
+    SplitParams shp = sp_;
+    shp.num_workers = nws;
+    shp.tiles = ws.shared_tiles;
+    shp.cum_pages = ws.cum_shared;
+    shp.batch = num_groups;
+    shp.part_ml = ws.shared_ml;
+    shp.part_acc = ws.shared_acc;
+    shp.unit_ml = ws.shared_unit_ml;
+    shp.unit_acc = ws.shared_unit_acc;
+    // Own-page pass: the single-unit workers.
     sp_.num_workers = nw;
     sp_.tiles = ws.own_tiles;
     sp_.cum_pages = ws.cum_own;
@@ -374,7 +374,9 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.part_acc = ws.own_acc;
     sp_.unit_ml = ws.own_unit_ml;
     sp_.unit_acc = ws.own_unit_acc;
-    if (launch_split(sp_, d->head_dim, false, d->stream) != hipSuccess)
+    if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
+        return SL_ERR_HIP;
+    if (launch_prefix_split(sp_, shp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
         return SL_ERR_HIP;

@@ -24,50 +24,27 @@
 // goes through an empty buffer resource and touches no memory), so the
 // compiler's counter waits stay exact and never drain the pipeline.
 //
+// The pass runs in the same launch as the own-page pass (prefix_split_kernel):
+// its workgroups share the CUs with the memory-bound single-unit workers, so
+// its latency- and MFMA-bound tiles are hidden under their streaming instead
+// of adding to it.
+//
 // Partial states: a unit cut by the range leaves its piece in worker slot
 // 2w (first piece) or 2w + 1 (trailing piece); a unit seen whole goes to its
 // own slot of the unit area, at (first query row) / G. Every state still has
 // to be merged with the members' own pages.
-#include "sl_internal.h"
+#include "decode_unit.h"
 
 namespace sl {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-
 constexpr int kSharedWaves = kPrefixBlocks;   // one wavefront per 16-row column block
-constexpr int kAhead = 3;                        // tiles in flight beyond the one computed
-constexpr float kNegInf = -__builtin_inff();
-// A partial state l = sum 2^(s - m), acc = sum 2^(s - m) v is exact for any
-// reference m; m is raised only when a score exceeds it by more than this
-// (base-2 units), so the weights stay below 2^8 and rescaling is rare.
-constexpr float kSlack = 8.0f;
-constexpr int kRawBufferWord3 = 0x00020000;   // untyped 32-bit buffer resource
+static_assert(kSharedWaves == kWavesPerBlock, "the fused prefix kernel runs both passes in one block shape");
+// Tiles in flight beyond the one computed. One is enough: the pass shares its
+// CUs with the memory-bound own-page workers, and a deeper ring (3) was
+// slower for the registers it took.
+constexpr int kAhead = 1;
 constexpr int kNonTemporal = 2;                // buffer cache policy: non-temporal (streamed once)
-
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
-{
-    f32x2_t v = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
-}
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
-__device__ __forceinline__ float quad_max(float x)
-{
-    x = fmaxf(x, __shfl_xor(x, 16, kWave));
-    return fmaxf(x, __shfl_xor(x, 32, kWave));
-}
-__device__ __forceinline__ float quad_sum(float x)
-{
-    x += __shfl_xor(x, 16, kWave);
-    return x + __shfl_xor(x, 32, kWave);
-}
 
 // Bytes of one K (or V) tile, of the quarter one wavefront loads, and the
 // per-lane load width.
@@ -173,7 +150,7 @@ __device__ __forceinline__ void compute(State<D> &st, const uint8_t *stage, cons
     for (int r = 0; r < 4; ++r)
         sc[r] = s4[r] * score_mul;
     const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-    if (mx > st.m + kSlack) {
+    if (mx > st.m + kRescaleSlack) {
         const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a piece's first tile
         st.l *= alpha;
 #pragma unroll
@@ -212,15 +189,13 @@ __device__ __forceinline__ void compute(State<D> &st, const uint8_t *stage, cons
     }
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) {
+        // Element i % 2 of dword i / 2 of rows 0 and 1 (lo) and rows 2 and 3
+        // (hi): one byte permute each (v_perm_b32 selects bytes of {a, b},
+        // selector bytes 4..7 from a, 0..3 from b).
         const int w = i >> 1;
-        uint32_t lo, hi;
-        if ((i & 1) == 0) {
-            lo = (vb[0 * RW + w] & 0xffffu) | (vb[1 * RW + w] << 16);
-            hi = (vb[2 * RW + w] & 0xffffu) | (vb[3 * RW + w] << 16);
-        } else {
-            lo = (vb[0 * RW + w] >> 16) | (vb[1 * RW + w] & 0xffff0000u);
-            hi = (vb[2 * RW + w] >> 16) | (vb[3 * RW + w] & 0xffff0000u);
-        }
+        const uint32_t sel = (i & 1) == 0 ? 0x05040100u : 0x07060302u;
+        const uint32_t lo = __builtin_amdgcn_perm(vb[1 * RW + w], vb[0 * RW + w], sel);
+        const uint32_t hi = __builtin_amdgcn_perm(vb[3 * RW + w], vb[2 * RW + w], sel);
         const i16x4_t va = __builtin_bit_cast(i16x4_t, u32x2_t{lo, hi});
         st.acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, st.acc[i], 0, 0, 0);
     }
@@ -280,10 +255,10 @@ __device__ __forceinline__ void load_q(bf16x8_t (&qop)[D / 32], const SplitParam
             bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(qr, rel * D * 2 + 2 * (32 * s + 8 * quad), 0, 0));
 }
 
+// Worker w (one workgroup) of the shared-page pass.
 template <int D>
-__global__ __launch_bounds__(kWave * kSharedWaves) void split_shared_kernel(SplitParams p)
+__device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w)
 {
-    const int w = blockIdx.x;
     const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
     const int nw = effective_workers(total, p.num_workers);
     if (w >= nw)
@@ -397,16 +372,34 @@ __global__ __launch_bounds__(kWave * kSharedWaves) void split_shared_kernel(Spli
     }
 }
 
+// Both passes of prefix-shared attention in one launch: workgroups
+// [0, own_blocks) run the single-unit workers of the own pages (four per
+// workgroup), the rest run shared-page workers. The own-page workgroups come
+// first, so each CU holds one of them beside a shared-page workgroup: the
+// memory-bound and the MFMA-heavy pass share the CUs instead of running one
+// after the other.
+template <int D>
+__global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(SplitParams own, SplitParams shared,
+                                                                               int own_blocks)
+{
+    if ((int)blockIdx.x < own_blocks)
+        split_unit_worker<D, false>(own,
+                                    blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
+    else
+        split_shared_worker<D>(shared, (int)blockIdx.x - own_blocks);
+}
+
 }  // namespace
 
-hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream)
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int head_dim, hipStream_t stream)
 {
-    const dim3 grid(p.num_workers);
-    const dim3 block(kWave * kSharedWaves);
+    const int own_blocks = (own.num_workers + kWavesPerBlock - 1) / kWavesPerBlock;
+    const dim3 grid(own_blocks + shared.num_workers);
+    const dim3 block(kWave * kWavesPerBlock);
     if (head_dim == 128)
-        hipLaunchKernelGGL(split_shared_kernel<128>, grid, block, 0, stream, p);
+        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, 0, stream, own, shared, own_blocks);
     else if (head_dim == 64)
-        hipLaunchKernelGGL(split_shared_kernel<64>, grid, block, 0, stream, p);
+        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, 0, stream, own, shared, own_blocks);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

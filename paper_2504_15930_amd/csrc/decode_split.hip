@@ -1,506 +1,15 @@
-// Split-KV decode attention kernel for gfx950.
-//
-// One wavefront is one worker. It streams its contiguous range of page-head
-// tiles (see sl_internal.h) as a flat sequence, keeping an online-softmax
-// state for the G query heads of the unit (sequence, KV head) the current tile
-// belongs to, and finishing that unit whenever its last tile, or the end of
-// the range, is reached.
-//
-// Per 16-token tile, with lane = n + 16 * quad (n = lane & 15, quad = lane >> 4):
-//
-//   scores  S^T[t][j] = sum_d K[t][d] Q[j][d]       v_mfma_f32_16x16x32_bf16
-//           A = K   (row t = n, 8 consecutive d per lane; the tile is read as
-//                    whole 1 KB runs and regrouped through LDS)
-//           B = Q^T (column j = n; query rows j >= G are zero padding)
-//           -> lane (j, quad) holds the scores of head j for tokens 4 quad + r
-//   softmax running max / sum per head j, kept in the lanes of column j: the
-//           only cross-lane step is a max over the four quads of a column
-//   values  O^T[d][j] += sum_t V[t][d] P[j][t]       v_mfma_f32_16x16x16bf16_1k
-//           A = V^T (lane (n, quad) holds V[4 quad + r][d_i(n)] for r = 0..3,
-//                    gathered from four 16-byte row loads and repacked)
-//           B = P^T exactly as the score MFMA left it (no data movement)
-//           -> lane (j, quad) accumulates O[j][d] for D/4 consecutive d
-//
-// V goes straight from HBM into MFMA operand registers: its loads already
-// cover whole 128-byte lines. The K operand layout would read only half a
-// line per instruction (each row spread over four lanes), which streams at
-// ~6.0 TB/s instead of ~6.85 TB/s on MI355X, so K is read in whole 1 KB runs
-// and regrouped through a small per-wave LDS buffer. Both are streamed with
-// non-temporal loads. Tiles are software-pipelined kNbuf deep;
-// the tile-list entry (page and unit metadata) of a tile is fetched one
-// pipeline turn before the tile itself, and the query rows of a unit are
-// loaded together with the unit's first tile, so the stream never waits on a
-// dependent load, also across unit boundaries.
-//
-// FP8 pages hold OCP E4M3 codes; they are widened to bf16 exactly
-// (v_cvt_scalef32_pk_bf16_fp8 with unit scale), the per-(page, head) key
-// scale multiplies the fp32 scores and the value scale multiplies the
-// probabilities before they are rounded for the value MFMA.
-#include "sl_internal.h"
+// Split-KV decode attention kernel for gfx950: one wavefront per worker, the
+// worker itself (tile pipeline, MFMA layout, online softmax, epilogue) is in
+// decode_unit.h.
+#include "decode_unit.h"
 
 namespace sl {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-
-constexpr float kNegInf = -__builtin_inff();
-// A partial state l = sum 2^(s - m), acc = sum 2^(s - m) v is exact for any
-// reference m. The running maximum is raised only when a score exceeds it by
-// more than this slack (base-2 units), which bounds the weights by 2^8 and
-// leaves the accumulators untouched on most tiles after a unit's first.
-constexpr float kRescaleSlack = 8.0f;
-#ifndef SL_NBUF
-#define SL_NBUF 2
-#endif
-constexpr int kNbuf = SL_NBUF;               // tiles in the software pipeline
-constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit buffer resource (CDNA3/4)
-
-__device__ __forceinline__ u32x4_t ld128(const uint8_t *p) { return *reinterpret_cast<const u32x4_t *>(p); }
-
-// K/V pages are read exactly once per call: stream them with non-temporal loads
-// so they do not displace reusable lines in L2 / the Infinity Cache (measured on
-// MI355X: random 4 KB tiles reach ~6.8 TB/s this way, ~6.0 TB/s with plain loads).
-__device__ __forceinline__ u32x4_t ld128_stream(const uint8_t *p)
-{
-    return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-}
-__device__ __forceinline__ u32x2_t ld64_stream(const uint8_t *p)
-{
-    return __builtin_nontemporal_load(reinterpret_cast<const u32x2_t *>(p));
-}
-__device__ __forceinline__ uint32_t ld32_stream(const uint8_t *p)
-{
-    return __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
-}
-
-// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
-{
-    f32x2_t v = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
-}
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
-
-// Four E4M3 codes (one dword) -> four bf16 (two dwords), exact.
-__device__ __forceinline__ void e4m3x4_to_bf16(uint32_t codes, uint32_t &lo, uint32_t &hi)
-{
-    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes, 1.0f, false));
-    hi = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes, 1.0f, true));
-}
-
-// Max / sum over the lanes n, n + 16, n + 32, n + 48 of a column.
-// (The gfx950 lane-swap builtins would avoid the LDS crossbar here, but this
-// compiler folds max(h[0], h[1]) of their two results to one of them, so the
-// plain shuffles are used.)
-__device__ __forceinline__ float quad_max(float x)
-{
-    x = fmaxf(x, __shfl_xor(x, 16, kWave));
-    return fmaxf(x, __shfl_xor(x, 32, kWave));
-}
-__device__ __forceinline__ float quad_sum(float x)
-{
-    x += __shfl_xor(x, 16, kWave);
-    return x + __shfl_xor(x, 32, kWave);
-}
-
-template <int D, bool FP8>
-struct Tile {
-    // Per-lane dwords of K (score-MFMA A operands) and V (four rows).
-    static constexpr int KW = FP8 ? D / 16 : D / 8;
-    static constexpr int VW = FP8 ? D / 16 : D / 8;
-    uint32_t k[KW];
-    uint32_t v[VW];
-    u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only
-    float scl;           // FP8: key scale in lanes 0-31, value scale in lanes 32-63
-    uint32_t meta;       // TileEntry::meta (wave-uniform)
-    bool bad_page;       // the block table named a page outside the pool
-};
-
-// Query element index held by (quad, item) in k-step s; must match k_operand.
-template <int D, bool FP8>
-__device__ __forceinline__ int q_index(int s, int quad)
-{
-    return FP8 ? quad * (D / 4) + 8 * s : 32 * s + 8 * quad;
-}
-
-// Issue every load of one tile. All loads are unconditional.
-template <int D, bool FP8>
-__device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p, int32_t page,
-                                           uint32_t meta, bool with_q, int n, int quad, int lane)
-{
-    constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
-    t.meta = meta;
-    t.bad_page = page < 0;
-    const size_t tile = (size_t)(page < 0 ? 0 : page);
-    const uint8_t *kt = static_cast<const uint8_t *>(p.k_pages) + tile * kTileBytes;
-    const uint8_t *vt = static_cast<const uint8_t *>(p.v_pages) + tile * kTileBytes;
-    // K: whole 1 KB runs per instruction (lane l reads bytes 16 l of each
-    // run), so every instruction covers complete 128-byte lines; the rows are
-    // regrouped into the score-MFMA layout through LDS when the tile is used.
-#pragma unroll
-    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
-        const u32x4_t x = ld128_stream(kt + 1024 * i + 16 * lane);
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            t.k[4 * i + c] = x[c];
-    }
-    if constexpr (!FP8) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint8_t *src = vt + ((4 * quad + r) * D + n * (D / 16)) * 2;
-            if constexpr (D == 128) {
-                const u32x4_t x = ld128_stream(src);
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    t.v[4 * r + c] = x[c];
-            } else {
-                const u32x2_t x = ld64_stream(src);
-                t.v[2 * r] = x[0];
-                t.v[2 * r + 1] = x[1];
-            }
-        }
-    } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint8_t *src = vt + (4 * quad + r) * D + n * (D / 16);
-            if constexpr (D == 128) {
-                const u32x2_t x = ld64_stream(src);
-                t.v[2 * r] = x[0];
-                t.v[2 * r + 1] = x[1];
-            } else {
-                t.v[r] = ld32_stream(src);
-            }
-        }
-        const float *sp = (lane & 32) ? p.v_scales : p.k_scales;
-        t.scl = sp[tile];
-    }
-    // The query rows of a unit travel with the unit's first tile (or the
-    // worker's first tile); lanes past the group read row G - 1 and are zeroed
-    // when the operand is formed.
-    if (with_q) {
-        const int G = p.group;
-        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s)
-            t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
-    }
-}
-
-// Regroup the K tile (loaded as whole 1 KB runs) into the score-MFMA layout
-// through this wave's LDS buffer: lane (t, quad) needs row t, and for bf16
-// the 16-byte chunks 4 s + quad (s = 0 .. D/32 - 1), for FP8 the D/64 chunks
-// starting at quad D/64. A chunk c of row r is stored at position
-// c ^ ((r / P) % C) of its row (P rows per 256 bytes, C chunks per row), which
-// makes the 16-lane groups of both the writes and the reads hit distinct banks.
-template <int D, bool FP8>
-__device__ __forceinline__ void regroup_k(const Tile<D, FP8> &t, uint8_t *lds, int lane, int n, int quad,
-                                          u32x4_t (&kc)[FP8 ? D / 64 : D / 32])
-{
-    constexpr int R = D * (FP8 ? 1 : 2);   // bytes per row
-    constexpr int C = R / 16;               // 16-byte chunks per row
-    constexpr int P = 256 / R;              // rows per 256 bytes
-#pragma unroll
-    for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
-        const int off = 1024 * i + 16 * lane;
-        const int r = off / R, c = (off % R) / 16;
-        *reinterpret_cast<u32x4_t *>(lds + r * R + 16 * (c ^ ((r / P) % C))) =
-            u32x4_t{t.k[4 * i], t.k[4 * i + 1], t.k[4 * i + 2], t.k[4 * i + 3]};
-    }
-    const int key = (n / P) % C;
-#pragma unroll
-    for (int s = 0; s < (FP8 ? D / 64 : D / 32); ++s) {
-        const int c = FP8 ? quad * (D / 64) + s : 4 * s + quad;
-        kc[s] = *reinterpret_cast<const u32x4_t *>(lds + n * R + 16 * (c ^ key));
-    }
-}
-
-// Score-MFMA A operand for k-step s (8 bf16 values of row t = n).
-template <int D, bool FP8>
-__device__ __forceinline__ bf16x8_t k_operand(const u32x4_t (&kc)[FP8 ? D / 64 : D / 32], int s)
-{
-    u32x4_t w;
-    if constexpr (!FP8) {
-        w = kc[s];
-    } else {
-        const uint32_t lo = kc[s / 2][2 * (s % 2)], hi = kc[s / 2][2 * (s % 2) + 1];
-        uint32_t a, b, c, d;
-        e4m3x4_to_bf16(lo, a, b);
-        e4m3x4_to_bf16(hi, c, d);
-        w = u32x4_t{a, b, c, d};
-    }
-    return __builtin_bit_cast(bf16x8_t, w);
-}
-
-template <int D>
-struct Piece {
-    f32x4_t acc[D / 16];
-    float m;   // running max of this lane's head, base-2 units
-    float l;   // this lane's share of the sum of (bf16-rounded) weights
-};
-
-template <int D>
-__device__ __forceinline__ void reset(Piece<D> &st)
-{
-#pragma unroll
-    for (int i = 0; i < D / 16; ++i)
-        st.acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    st.m = kNegInf;
-    st.l = 0.f;
-}
-
-// One tile of the online softmax. `valid` = live tokens in this page (1..16).
-template <int D, bool FP8>
-__device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t,
-                                             const bf16x8_t (&qop)[D / 32], float score_mul,
-                                             int valid, uint8_t *lds, int lane, int n, int quad)
-{
-    u32x4_t kc[FP8 ? D / 64 : D / 32];
-    regroup_k<D, FP8>(t, lds, lane, n, quad, kc);
-    f32x4_t s4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s)
-        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<D, FP8>(kc, s), qop[s], s4, 0, 0, 0);
-
-    float vmul = 1.0f;
-    if constexpr (FP8) {
-        const int bits = __builtin_bit_cast(int, t.scl);
-        score_mul *= __builtin_bit_cast(float, __builtin_amdgcn_readlane(bits, 0));
-        vmul = __builtin_bit_cast(float, __builtin_amdgcn_readlane(bits, 32));
-    }
-    float sc[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-        sc[r] = s4[r] * score_mul;
-    if (valid < kPageSize) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            if (4 * quad + r >= valid)
-                sc[r] = kNegInf;
-    }
-    const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-    if (mx > st.m + kRescaleSlack) {
-        const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a unit's first tile
-        st.l *= alpha;
-#pragma unroll
-        for (int i = 0; i < D / 16; ++i)
-            st.acc[i] *= alpha;
-        st.m = mx;
-    }
-    float pr[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-        pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
-    const uint32_t p01 = pack_bf16(pr[0], pr[1]);
-    const uint32_t p23 = pack_bf16(pr[2], pr[3]);
-    st.l += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
-    i16x4_t pb;
-    if constexpr (FP8) {
-        const uint32_t w01 = pack_bf16(pr[0] * vmul, pr[1] * vmul);
-        const uint32_t w23 = pack_bf16(pr[2] * vmul, pr[3] * vmul);
-        pb = __builtin_bit_cast(i16x4_t, u32x2_t{w01, w23});
-    } else {
-        pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
-    }
-
-    // Value rows as bf16 dwords: row r holds D/16 consecutive elements.
-    constexpr int RW = D / 32;   // bf16 dwords per row
-    uint32_t vb[4 * RW];
-    if constexpr (FP8) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int c = 0; c < D / 64; ++c)
-                e4m3x4_to_bf16(t.v[r * (D / 64) + c], vb[r * RW + 2 * c], vb[r * RW + 2 * c + 1]);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4 * RW; ++i)
-            vb[i] = t.v[i];
-    }
-    uint32_t mlo = 0xffffffffu, mhi = 0xffffffffu;
-    if (valid < kPageSize) {   // zero dead rows: their slots may hold NaN
-        const int t0 = 4 * quad;
-        mlo = (t0 + 0 < valid ? 0x0000ffffu : 0u) | (t0 + 1 < valid ? 0xffff0000u : 0u);
-        mhi = (t0 + 2 < valid ? 0x0000ffffu : 0u) | (t0 + 3 < valid ? 0xffff0000u : 0u);
-    }
-#pragma unroll
-    for (int i = 0; i < D / 16; ++i) {
-        const int w = i >> 1;
-        uint32_t lo, hi;
-        if ((i & 1) == 0) {
-            lo = (vb[0 * RW + w] & 0xffffu) | (vb[1 * RW + w] << 16);
-            hi = (vb[2 * RW + w] & 0xffffu) | (vb[3 * RW + w] << 16);
-        } else {
-            lo = (vb[0 * RW + w] >> 16) | (vb[1 * RW + w] & 0xffff0000u);
-            hi = (vb[2 * RW + w] >> 16) | (vb[3 * RW + w] & 0xffff0000u);
-        }
-        const i16x4_t va = __builtin_bit_cast(i16x4_t, u32x2_t{lo & mlo, hi & mhi});
-        st.acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, st.acc[i], 0, 0, 0);
-    }
-}
-
-// Finish the current unit: normalise and write its bf16 rows if the whole unit
-// was seen and nothing else is merged into it (`full`), else store the partial
-// state, G rows, in slot `slot` of (part_ml, part_acc).
-template <int D>
-__device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, uint32_t row0, bool full,
-                                            bool bad, float *part_ml, float *part_acc, size_t slot, int n,
-                                            int quad)
-{
-    const int G = p.group;
-    const float l = quad_sum(st.l);
-    const int d0 = quad * (D / 4);   // this lane holds O[row0 + n][d0 .. d0 + D/4)
-    if (n >= G)
-        return;
-    if (full) {
-        const float inv = bad ? __builtin_nanf("") : 1.0f / l;
-        uint8_t *dst = reinterpret_cast<uint8_t *>(p.out + ((size_t)row0 + n) * D + d0);
-#pragma unroll
-        for (int c = 0; c < D / 32; ++c) {
-            // output columns d0 + 8c .. 8c + 7 are acc[i][r] with r * D/16 + i = 8c + ...
-            uint32_t wv[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int k0 = 8 * c + 2 * e;   // flat index r * (D/16) + i
-                const int r0 = k0 / (D / 16), i0 = k0 % (D / 16);
-                const int k1 = k0 + 1;
-                const int r1 = k1 / (D / 16), i1 = k1 % (D / 16);
-                wv[e] = pack_bf16(st.acc[i0][r0] * inv, st.acc[i1][r1] * inv);
-            }
-            *reinterpret_cast<u32x4_t *>(dst + 16 * c) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
-        }
-    } else {
-        const float poison = bad ? __builtin_nanf("") : 0.0f;
-        float *dst = part_acc + (slot * G + n) * D + d0;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int i = 0; i < D / 16; i += 4)
-                *reinterpret_cast<f32x4_t *>(dst + r * (D / 16) + i) =
-                    f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
-        if (quad == 0)   // a NaN maximum keeps the poison alive through the merge weights
-            *reinterpret_cast<f32x2_t *>(part_ml + (slot * G + n) * 2) =
-                f32x2_t{st.m + poison, l};
-    }
-}
-
 template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
-    const int w = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    if (w >= p.num_workers)
-        return;
-    const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
-    const int nw = effective_workers(total, p.num_workers);
-    if (w >= nw)
-        return;
-    const long long s0 = (long long)w * total / nw;
-    const long long s1 = (long long)(w + 1) * total / nw;
-    if (s0 >= s1)
-        return;
-    const int ntiles = (int)(s1 - s0);
-    const int lane = threadIdx.x & (kWave - 1);
-    const int n = lane & 15;
-    const int quad = lane >> 4;
-    const int G = p.group;
-    // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
-    __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
-    uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
-
-    // This worker's tile-list entries, read through a bounds-checked buffer
-    // resource; an index past the range is clamped to the last tile.
-    const __amdgpu_buffer_rsrc_t ents = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<TileEntry *>(p.tiles + s0), 0, ntiles * (int)sizeof(TileEntry), kRawBufferWord3);
-    auto entry = [&](int i) -> u32x2_t {
-        const int j = i < ntiles ? i : ntiles - 1;
-        return __builtin_bit_cast(
-            u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
-    };
-    auto page_of = [](u32x2_t e) { return (int32_t)__builtin_amdgcn_readfirstlane(e[0]); };
-    auto meta_of = [](u32x2_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
-
-    // Ring of entries: slot k holds the entry of the tile issued at step k (mod
-    // kNbuf). The first entries and the ring are fetched together and waited
-    // for once here (the empty asm consumes them), so that inside the loop the
-    // counter wait for an entry only ever covers the loads of one pipeline turn
-    // and never drains the pipeline.
-    u32x2_t first[kNbuf - 1];
-#pragma unroll
-    for (int k = 0; k < kNbuf - 1; ++k)
-        first[k] = entry(k);
-    u32x2_t ring[kNbuf];
-#pragma unroll
-    for (int k = 0; k < kNbuf; ++k)
-        ring[k] = entry(kNbuf - 1 + k);
-#pragma unroll
-    for (int k = 0; k < kNbuf; ++k)
-        asm volatile("" ::"v"(ring[k]));
-    int32_t first_page[kNbuf - 1];
-    uint32_t first_meta[kNbuf - 1];
-#pragma unroll
-    for (int k = 0; k < kNbuf - 1; ++k) {
-        first_page[k] = page_of(first[k]);
-        first_meta[k] = meta_of(first[k]);
-    }
-
-    Tile<D, FP8> buf[kNbuf];
-#pragma unroll
-    for (int k = 0; k < kNbuf - 1; ++k)
-        issue_tile<D, FP8>(buf[k], p, first_page[k], first_meta[k],
-                           k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane);
-
-    Piece<D> st;
-    reset(st);
-    bf16x8_t qop[D / 32];   // score-MFMA B operands of the current unit (zero columns past its rows)
-    bool started = false;   // the current unit's first tile is inside this range
-    bool bad = false;
-    int slot_sel = 0;
-    for (int i0 = 0; i0 < ntiles; i0 += kNbuf) {
-#pragma unroll
-        for (int k = 0; k < kNbuf; ++k) {
-            const int i = i0 + k;
-            const uint32_t next_meta = meta_of(ring[k]);
-            issue_tile<D, FP8>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
-                               (next_meta & kMetaFirst) != 0, n, quad, lane);
-            ring[k] = entry(i + 2 * kNbuf - 1);
-            if (i < ntiles) {
-                const Tile<D, FP8> &t = buf[k];
-                const uint32_t meta = t.meta;
-                if (i == 0 || (meta & kMetaFirst) != 0) {
-#pragma unroll
-                    for (int s = 0; s < D / 32; ++s)
-                        qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
-                }
-                started |= (meta & kMetaFirst) != 0;
-                bad |= t.bad_page || (meta & kMetaBadLen) != 0;
-                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n, quad);
-                if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
-                    // A unit cut by this range leaves its piece in the worker's slot 2w + slot_sel.
-                    // A whole unit is written out, unless it still has to be merged (shared pages,
-                    // or the own pages of a sequence that has them): then its state goes to its
-                    // own slot in the unit area, indexed by (first query row) / G.
-                    const uint32_t row0 = meta >> kMetaRowShift;
-                    const bool whole = started && (meta & kMetaLast) != 0;
-                    const bool to_unit = whole && (meta & kMetaPrefixed) != 0;
-                    float *const pml = to_unit ? p.unit_ml : p.part_ml;
-                    float *const pacc = to_unit ? p.unit_acc : p.part_acc;
-                    const size_t slot = to_unit ? (size_t)(row0 / (uint32_t)G) : 2 * (size_t)w + slot_sel;
-                    finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
-                    reset(st);
-                    started = false;
-                    bad = false;
-                    slot_sel = 1;
-                }
-            }
-        }
-    }
+    split_unit_worker<D, FP8>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
 }
 
 }  // namespace

@@ -187,10 +187,11 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
 
 hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
-// Prefix mode: the shared pass (one workgroup of kPrefixBlocks wavefronts per
-// worker, one 16-row column block each; partial states only; p.num_workers
-// counts workgroups) and the partitioner / merge around the two passes.
-hipError_t launch_split_shared(const SplitParams &p, int head_dim, hipStream_t stream);
+// Prefix mode: the own-page pass (single-unit workers) and the shared-page
+// pass (one workgroup of kPrefixBlocks wavefronts per worker, one 16-row
+// column block each, partial states only; shared.num_workers counts
+// workgroups) in one launch, and the partitioner / merge around them.
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int head_dim, hipStream_t stream);
 hipError_t launch_partition_prefix(const PrefixPartitionParams &p, hipStream_t stream);
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
