@@ -1,6 +1,7 @@
 // Host side of libsl: argument checks, workspace layout, launch geometry and
-// the three launches of one decode-attention call (partition -> split-KV ->
-// merge), all enqueued on the caller's stream with no host synchronisation.
+// the launches of one decode-attention call (split-KV with its own work
+// partition -> merge; prefix sharing: partition -> fused split -> merge), all
+// enqueued on the caller's stream with no host synchronisation.
 #include <mutex>
 
 #include "../../include/sl.h"
@@ -22,8 +23,6 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
     };
     Workspace w;
     w.cum_pages = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
-    w.tiles = reinterpret_cast<TileEntry *>(
-        take(sizeof(TileEntry) * (size_t)batch * max_blocks * num_kv_heads));
     w.part_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
     w.part_acc = reinterpret_cast<float *>(
         take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
@@ -188,26 +187,15 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
         (reinterpret_cast<uintptr_t>(d->workspace) & (kAlign - 1)) != 0)
         return SL_ERR_WORKSPACE;
 
-    PartitionParams pp;
-    pp.seq_lens = seq_lens;
-    pp.block_table = block_table;
-    pp.cum_pages = ws.cum_pages;
-    pp.tiles = ws.tiles;
-    pp.batch = d->batch;
-    pp.num_q_heads = d->num_q_heads;
-    pp.num_kv_heads = d->num_kv_heads;
-    pp.max_blocks = d->max_blocks_per_seq;
-    pp.num_pages = d->num_pages;
-    if (launch_partition(pp, d->stream) != hipSuccess)
-        return SL_ERR_HIP;
-
+    // The split kernel partitions the work itself (direct mode): each
+    // workgroup scans the lengths into LDS and walks the block table.
     SplitParams sp;
     sp.q = q;
     sp.k_pages = k_pages;
     sp.v_pages = v_pages;
     sp.k_scales = k_scales;
     sp.v_scales = v_scales;
-    sp.tiles = ws.tiles;
+    sp.tiles = nullptr;   // direct mode
     sp.cum_pages = ws.cum_pages;
     sp.out = out;
     sp.part_ml = ws.part_ml;
@@ -220,6 +208,11 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     sp.num_q_heads = d->num_q_heads;
     sp.unit_ml = nullptr;
     sp.unit_acc = nullptr;
+    sp.seq_lens = seq_lens;
+    sp.block_table = block_table;
+    sp.cum_out = ws.cum_pages;
+    sp.max_blocks = d->max_blocks_per_seq;
+    sp.num_pages = d->num_pages;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (launch_split(sp, d->head_dim, fp8, d->stream) != hipSuccess)
@@ -354,6 +347,11 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.num_workers = nw;
     sp_.num_q_heads = d->num_q_heads;
     sp_.scale_log2 = scale * 1.4426950408889634f;
+    sp_.seq_lens = seq_lens;
+    sp_.block_table = block_table;
+    sp_.cum_out = nullptr;   // tile-list mode
+    sp_.max_blocks = d->max_blocks_per_seq;
+    sp_.num_pages = d->num_pages;
     // Shared-page pass: one workgroup of four wavefronts per worker.
     const int nws = shared_workers(nw);
     SplitParams shp = sp_;

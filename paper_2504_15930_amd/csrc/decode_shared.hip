@@ -383,8 +383,8 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(Sp
                                                                                int own_blocks)
 {
     if ((int)blockIdx.x < own_blocks)
-        split_unit_worker<D, false>(own,
-                                    blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
+        split_unit_worker<D, false, false>(
+            own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), nullptr);
     else
         split_shared_worker<D>(shared, (int)blockIdx.x - own_blocks);
 }

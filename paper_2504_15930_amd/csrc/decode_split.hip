@@ -6,10 +6,14 @@
 namespace sl {
 namespace {
 
+// Direct mode: every workgroup derives the tile stream from the lengths and
+// the block table (its dynamic LDS holds the page prefix sum and the lengths).
 template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
-    split_unit_worker<D, FP8>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
+    extern __shared__ int32_t s_dyn[];
+    split_unit_worker<D, FP8, true>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+                                    s_dyn);
 }
 
 }  // namespace
@@ -18,14 +22,15 @@ hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_
 {
     const dim3 grid((p.num_workers + kWavesPerBlock - 1) / kWavesPerBlock);
     const dim3 block(kWave * kWavesPerBlock);
+    const size_t lds = split_dynamic_lds(p.batch);
     if (head_dim == 128 && !fp8)
-        hipLaunchKernelGGL((split_kv_kernel<128, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((split_kv_kernel<128, false>), grid, block, lds, stream, p);
     else if (head_dim == 64 && !fp8)
-        hipLaunchKernelGGL((split_kv_kernel<64, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((split_kv_kernel<64, false>), grid, block, lds, stream, p);
     else if (head_dim == 128 && fp8)
-        hipLaunchKernelGGL((split_kv_kernel<128, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((split_kv_kernel<128, true>), grid, block, lds, stream, p);
     else if (head_dim == 64 && fp8)
-        hipLaunchKernelGGL((split_kv_kernel<64, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((split_kv_kernel<64, true>), grid, block, lds, stream, p);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

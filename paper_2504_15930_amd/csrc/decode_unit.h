@@ -393,13 +393,71 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
     }
 }
 
-// Worker w (one wavefront) of the single-unit split-KV pass.
-template <int D, bool FP8>
-__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w)
+// Direct mode, run by the whole workgroup before its workers start: the
+// pages per sequence n_b = ceil(clamp(L_b, 0, max_blocks * 16) / 16), their
+// exclusive prefix sum in s_cum[0 .. B] and the lengths in s_len[0 .. B), all
+// in LDS; workgroup 0 also stores the prefix sum for the merge.
+__device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_cum, int32_t *s_len)
 {
+    __shared__ int32_t s_wave[kWavesPerBlock];
+    constexpr int T = kWave * kWavesPerBlock;
+    const int B = p.batch;
+    const int tid = threadIdx.x;
+    const int max_len = p.max_blocks * kPageSize;
+    const int per = (B + T - 1) / T;
+    const int lo = min(B, tid * per), hi = min(B, lo + per);
+    int local = 0;
+    for (int b = lo; b < hi; ++b) {
+        const int L = p.seq_lens[b];
+        const int nb = L <= 0 ? 0 : (min(L, max_len) + kPageSize - 1) / kPageSize;
+        s_len[b] = L;
+        s_cum[b] = nb;
+        local += nb;
+    }
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    int incl = local;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int v = __shfl_up(incl, off, kWave);
+        if (lane >= off)
+            incl += v;
+    }
+    if (lane == kWave - 1)
+        s_wave[wave] = incl;
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < kWavesPerBlock; ++k) {
+        base += k < wave ? s_wave[k] : 0;
+        total += s_wave[k];
+    }
+    int run = base + incl - local;
+    for (int b = lo; b < hi; ++b) {
+        const int nb = s_cum[b];
+        s_cum[b] = run;
+        run += nb;
+    }
+    if (tid == 0)
+        s_cum[B] = total;
+    __syncthreads();
+    if (blockIdx.x == 0)
+        for (int b = tid; b <= B; b += T)
+            p.cum_out[b] = s_cum[b];
+}
+
+// Worker w (one wavefront) of the single-unit split-KV pass. With DIRECT the
+// tiles come from the lengths and the block table (s_dyn: 2 B + 1 ints of
+// LDS, and the whole workgroup must call this); otherwise from the tile list.
+template <int D, bool FP8, bool DIRECT>
+__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, int32_t *s_dyn)
+{
+    int32_t *const s_cum = s_dyn;
+    int32_t *const s_len = s_dyn + p.batch + 1;
+    if constexpr (DIRECT)
+        scan_sequences(p, s_cum, s_len);
     if (w >= p.num_workers)
         return;
-    const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
+    const long long total = (long long)(DIRECT ? s_cum[p.batch] : p.cum_pages[p.batch]) * p.num_kv_heads;
     const int nw = effective_workers(total, p.num_workers);
     if (w >= nw)
         return;
@@ -416,28 +474,91 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w)
     __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 
-    // This worker's tile-list entries, read through a bounds-checked buffer
-    // resource; an index past the range is clamped to the last tile.
+    // Tile entries, fetched in tile order (every call below asks for the next
+    // tile; past the range the last tile repeats). An entry is {page-head tile
+    // index, or -1 for a page outside the pool; metadata}, read from the tile
+    // list through a bounds-checked buffer resource, or in direct mode {block-
+    // table entry (loaded), metadata and KV head (from a cursor over the
+    // units)}.
     const __amdgpu_buffer_rsrc_t ents = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<TileEntry *>(p.tiles + s0), 0, ntiles * (int)sizeof(TileEntry), kRawBufferWord3);
-    auto entry = [&](int i) -> u32x2_t {
-        const int j = i < ntiles ? i : ntiles - 1;
-        return __builtin_bit_cast(
-            u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
+    const __amdgpu_buffer_rsrc_t btab = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(p.block_table), 0, p.batch * p.max_blocks * (int)sizeof(int32_t), kRawBufferWord3);
+    // Direct-mode cursor: tile (b, g, j) of the stream, n_b and L_b.
+    int cb = 0, cg = 0, cj = 0, cnb = 0, clen = 0;
+    if constexpr (DIRECT) {
+        // Largest b with Hkv cum[b] <= s0 (then its n_b > 0).
+        int blo = 0, bhi = p.batch;
+        while (bhi - blo > 1) {
+            const int mid = (blo + bhi) >> 1;
+            if ((long long)s_cum[mid] * p.num_kv_heads <= s0)
+                blo = mid;
+            else
+                bhi = mid;
+        }
+        cb = blo;
+        cnb = s_cum[cb + 1] - s_cum[cb];
+        clen = s_len[cb];
+        const int off = (int)(s0 - (long long)s_cum[cb] * p.num_kv_heads);
+        cg = off / cnb;
+        cj = off - cg * cnb;
+    }
+    const int max_len = p.max_blocks * kPageSize;
+    auto entry = [&](int i) -> u32x4_t {
+        if constexpr (!DIRECT) {
+            const int j = i < ntiles ? i : ntiles - 1;
+            const u32x2_t e = __builtin_bit_cast(
+                u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
+            return u32x4_t{e[0], e[1], 0u, 0u};
+        } else {
+            const uint32_t bt = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (cb * p.max_blocks + cj) * 4, 0));
+            const int live = min(kPageSize, clen - cj * kPageSize);
+            uint32_t meta = (uint32_t)(max(live, 1) - 1) |
+                            ((uint32_t)(cb * p.num_q_heads + cg * G) << kMetaRowShift);
+            if (cj == 0)
+                meta |= kMetaFirst;
+            if (cj == cnb - 1)
+                meta |= kMetaLast;
+            if (clen > max_len)
+                meta |= kMetaBadLen;
+            const u32x4_t e = {bt, meta, (uint32_t)cg, 0u};
+            if (i < ntiles - 1) {   // advance to the next tile of the stream
+                if (++cj == cnb) {
+                    cj = 0;
+                    if (++cg == p.num_kv_heads) {
+                        cg = 0;
+                        do
+                            ++cb;
+                        while (s_cum[cb + 1] == s_cum[cb]);   // tiles remain, so a sequence with pages follows
+                        cnb = s_cum[cb + 1] - s_cum[cb];
+                        clen = s_len[cb];
+                    }
+                }
+            }
+            return e;
+        }
     };
-    auto page_of = [](u32x2_t e) { return (int32_t)__builtin_amdgcn_readfirstlane(e[0]); };
-    auto meta_of = [](u32x2_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
+    auto page_of = [&](u32x4_t e) -> int32_t {
+        if constexpr (!DIRECT) {
+            return (int32_t)__builtin_amdgcn_readfirstlane(e[0]);
+        } else {
+            const uint32_t bt = (uint32_t)__builtin_amdgcn_readfirstlane(e[0]);
+            return bt < (uint32_t)p.num_pages ? (int32_t)(bt * (uint32_t)p.num_kv_heads + e[2]) : -1;
+        }
+    };
+    auto meta_of = [](u32x4_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
 
     // Ring of entries: slot k holds the entry of the tile issued at step k (mod
     // kNbuf). The first entries and the ring are fetched together and waited
     // for once here (the empty asm consumes them), so that inside the loop the
     // counter wait for an entry only ever covers the loads of one pipeline turn
     // and never drains the pipeline.
-    u32x2_t first[kNbuf - 1];
+    u32x4_t first[kNbuf - 1];
 #pragma unroll
     for (int k = 0; k < kNbuf - 1; ++k)
         first[k] = entry(k);
-    u32x2_t ring[kNbuf];
+    u32x4_t ring[kNbuf];
 #pragma unroll
     for (int k = 0; k < kNbuf; ++k)
         ring[k] = entry(kNbuf - 1 + k);

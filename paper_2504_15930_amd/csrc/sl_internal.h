@@ -1,6 +1,7 @@
 // Internal interface between the host-side entry points (api.cpp) and the
-// gfx950 kernels (partition.hip, decode_split.hip, merge.hip, append.hip,
-// engine.hip), and the decode engine (engine.cpp).
+// gfx950 kernels (decode_split.hip with the worker in decode_unit.h,
+// decode_shared.hip, partition.hip, merge.hip, append.hip, engine.hip), and
+// the decode engine (engine.cpp).
 //
 // Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
 // n_b = ceil(L_b / 16) page-head tiles (16 tokens x head_dim of one KV head).
@@ -12,9 +13,14 @@
 // chip idle (the on-chip analogue of StreamRL's skewness bubbles, Section 2.4
 // and Section 5.1).
 //
-// The partitioner writes one 8-byte entry per tile (TileEntry), so a worker
-// streams its range as one flat sequence of tiles: unit boundaries inside the
-// range cost no dependent load and do not drain the load pipeline.
+// A worker streams its range as one flat sequence of tiles. In plain decode
+// attention each workgroup derives the stream itself: it scans the lengths
+// into LDS, locates its workers' first tiles by binary search and walks the
+// block table with a cursor (direct mode). Prefix-shared attention streams
+// tile lists of one 8-byte entry per tile (TileEntry), written by its
+// partitioner. Either way the entry of a tile is fetched a pipeline turn
+// ahead, so unit boundaries inside the range cost no dependent load and do
+// not drain the load pipeline.
 //
 // A unit that lies inside one worker's range is finished by that worker; a
 // unit cut by a range boundary leaves one partial softmax state per worker
@@ -34,7 +40,7 @@ constexpr int kPageSize = 16;
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;          // split kernel: 4 independent workers per block
 constexpr int kMaxGroup = 16;              // query heads per KV head (one MFMA column block)
-constexpr int kMaxBatch = 8192;            // the partitioner keeps one int per sequence in LDS
+constexpr int kMaxBatch = 8192;            // the split kernel keeps two ints per sequence in LDS
 constexpr int kPartitionThreads = 1024;
 constexpr int kMergeThreads = 256;         // one wave per unit, four units per block
 constexpr int kMaxWorkers = 1 << 16;       // keeps partial-state offsets below 2^31 bytes
@@ -80,18 +86,9 @@ constexpr int kPrefixRows = 16 * kPrefixBlocks;
 constexpr int kMetaRowShift = 8;
 
 struct Workspace {
-    int32_t *cum_pages;   // [B + 1] exclusive prefix sum of pages per sequence
-    TileEntry *tiles;     // [B * max_blocks * Hkv] (the first W are used)
+    int32_t *cum_pages;   // [B + 1] exclusive prefix sum of pages per sequence (written by the split kernel)
     float *part_ml;       // [2 NW][G][2]  (running max in log2 units, sum of weights)
     float *part_acc;      // [2 NW][G][D]  un-normalised weighted value sums
-};
-
-struct PartitionParams {
-    const int32_t *seq_lens;
-    const int32_t *block_table;
-    int32_t *cum_pages;
-    TileEntry *tiles;
-    int32_t batch, num_q_heads, num_kv_heads, max_blocks, num_pages;
 };
 
 struct SplitParams {
@@ -114,6 +111,13 @@ struct SplitParams {
     // row stride of part_ml / part_acc; null otherwise.
     float *unit_ml;
     float *unit_acc;
+    // Direct mode (no tile list): the kernel derives every tile from the
+    // lengths and the block table itself, and workgroup 0 stores the page
+    // prefix sum in cum_out for the merge.
+    const int32_t *seq_lens;
+    const int32_t *block_table;
+    int32_t *cum_out;
+    int32_t max_blocks, num_pages;
 };
 
 // Prefix-sharing mode. Groups are runs of consecutive sequences
@@ -185,7 +189,9 @@ size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv
 size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
                         int head_dim, int num_workers, Workspace *ws);
 
-hipError_t launch_partition(const PartitionParams &p, hipStream_t stream);
+// The direct-mode split kernel's dynamic LDS: the page prefix sum (B + 1
+// ints) and the lengths (B ints).
+inline size_t split_dynamic_lds(int batch) { return sizeof(int32_t) * (2 * (size_t)batch + 1); }
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Prefix mode: the own-page pass (single-unit workers) and the shared-page
 // pass (one workgroup of kPrefixBlocks wavefronts per worker, one 16-row
