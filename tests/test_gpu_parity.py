@@ -63,6 +63,20 @@ def test_random_shapes(shape, workers, kv):
     assert_parity(out, oracle_full(b), f"{shape} workers={workers} {kv}")
 
 
+@pytest.mark.parametrize("workers", [1, 3, 16, 97, 1000, 0])
+def test_sparse_batch_with_empty_runs(workers):
+    """Mostly empty sequences, including the first and the last, with the non-empty ones far apart:
+    every worker locates its first tile by binary search over runs of equal page prefix sums and
+    walks across the empty sequences between units."""
+    _say("sparse batch workers", workers)
+    L = np.zeros(64, np.int64)
+    L[[5, 6, 31, 47, 62]] = [33, 1, 700, 16, 257]
+    b = inputs.make_paged_batch(L, 28, 4, 128, seed=11, device=DEV)
+    out = sl.run_batch(b, num_workers=workers)
+    torch.cuda.synchronize()
+    assert_parity(out, oracle_full(b), f"sparse workers={workers}")
+
+
 @pytest.mark.parametrize("workers", [1, 2, 3, 7, 16, 64, 1000, 0])
 def test_worker_count_independence(workers):
     _say("worker count", workers)
