@@ -22,7 +22,8 @@
  * page; a finished sample's pages return to the stack last block first.
  *
  * Every step, on desc.stream and in this order: the step's sequence lengths
- * and new block-table entries are copied to the device and applied; new
+ * and new block-table entries are read by the device from a mapped pinned
+ * staging buffer and applied; new
  * prompt pages are filled; sl_kv_append stores the step's new K/V rows (the
  * caller's k_new / v_new buffers, the same every step); sl_decode_attn (or
  * _fp8) computes the step's attention output into `out` with the caller's q.
@@ -30,12 +31,13 @@
  *
  * The schedule is fixed by the lengths given at creation, so the host never
  * waits for the device during a run: steps are enqueued asynchronously, and
- * the host only waits for the copy of a staging buffer it is about to reuse.
+ * the host only waits for the kernels that read a staging buffer it is about
+ * to reuse.
  *
  * Memory: all buffers in sl_engine_buffers are the caller's; the engine keeps
  * their pointers until sl_engine_destroy. The engine allocates, at creation
- * only, one device staging buffer and a small ring of pinned host buffers,
- * released by sl_engine_destroy.
+ * only, a small ring of mapped pinned host buffers for its staging, released
+ * by sl_engine_destroy.
  */
 #ifndef SL_ENGINE_H
 #define SL_ENGINE_H

@@ -4,10 +4,12 @@
 // into BS slots, pages come from a LIFO free stack, and the lengths given at
 // creation fix every step in advance. Each step is packed into a pinned
 // staging buffer ([seq_lens][block-table updates][prompt pages to fill]),
-// copied to the device asynchronously and followed by four launches on the
+// followed by four launches on the
 // caller's stream: apply, fill (only when a prompt was admitted), KV append
-// and decode attention. A ring of pinned buffers, each reused only once the
-// copy that read it has completed, lets the host run ahead of the GPU.
+// and decode attention. The apply and fill kernels read the staging buffer in
+// place (mapped pinned memory), which saves a copy command per step; a ring of
+// such buffers, each reused only once the kernels that read it have
+// completed, lets the host run ahead of the GPU.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -43,9 +45,9 @@ struct sl_engine {
     int step = 0;
     bool done = false;
     sl_status failed = SL_OK;
-    int32_t *d_stage = nullptr;
     size_t stage_ints = 0;
-    int32_t *h_stage[kRing] = {};
+    int32_t *h_stage[kRing] = {};   // mapped pinned staging buffers
+    int32_t *d_stage[kRing] = {};   // their device addresses
     hipEvent_t ev[kRing] = {};
     bool ev_pending[kRing] = {};
     int ring = 0;
@@ -58,8 +60,6 @@ struct sl_engine {
             if (h_stage[r])
                 (void)hipHostFree(h_stage[r]);
         }
-        if (d_stage)
-            (void)hipFree(d_stage);
     }
 
     sl_status one_step();
@@ -121,18 +121,17 @@ sl_status sl_engine::one_step()
     const int n_fill = (int)fills.size();
     std::memcpy(h + BS, upd.data(), sizeof(int32_t) * upd.size());
     std::memcpy(h + BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
-    const size_t ints = BS + upd.size() + fills.size();
     hipStream_t s = step_desc.stream;
-    if (hipMemcpyAsync(d_stage, h, sizeof(int32_t) * ints, hipMemcpyHostToDevice, s) != hipSuccess ||
-        hipEventRecord(ev[r], s) != hipSuccess)
-        return SL_ERR_HIP;
-    ev_pending[r] = true;
-    if (sl::launch_engine_apply(d_stage, BS, n_upd, max_blocks, buf.seq_lens, buf.block_table, s) != hipSuccess)
+    const int32_t *ds = d_stage[r];
+    if (sl::launch_engine_apply(ds, BS, n_upd, max_blocks, buf.seq_lens, buf.block_table, s) != hipSuccess)
         return SL_ERR_HIP;
     if (n_fill > 0 &&
-        sl::launch_engine_fill(d_stage + BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
+        sl::launch_engine_fill(ds + BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
                                buf.k_scales, buf.v_scales, s) != hipSuccess)
         return SL_ERR_HIP;
+    if (hipEventRecord(ev[r], s) != hipSuccess)   // the staging buffer is free again after this
+        return SL_ERR_HIP;
+    ev_pending[r] = true;
     sl_status st;
     if (fp8) {
         st = sl_kv_append_fp8(&step_desc, buf.k_new, buf.v_new, buf.block_table, buf.seq_lens,
@@ -248,10 +247,11 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     e->finish.assign(M, -1);
     // staging: lengths, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
     e->stage_ints = (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
-    bool ok = hipMalloc(&e->d_stage, sizeof(int32_t) * e->stage_ints) == hipSuccess;
+    bool ok = true;
     for (int r = 0; ok && r < kRing; ++r)
         ok = hipHostMalloc(reinterpret_cast<void **>(&e->h_stage[r]), sizeof(int32_t) * e->stage_ints,
-                           hipHostMallocDefault) == hipSuccess &&
+                           hipHostMallocMapped) == hipSuccess &&
+             hipHostGetDevicePointer(reinterpret_cast<void **>(&e->d_stage[r]), e->h_stage[r], 0) == hipSuccess &&
              hipEventCreateWithFlags(&e->ev[r], hipEventDisableTiming) == hipSuccess;
     if (!ok) {
         e->release();
