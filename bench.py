@@ -451,7 +451,8 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "e4m3 KV, bf16 q/out, fp32 accumulate" if kvb == 1 else "bf16 (fp32 accumulate)",
+        "dtype": "e4m3" if kvb == 1 else "bf16",
+        "accumulate": "f32",
         "data": "synthetic",
         "config": {
             "workload": args.workload,
