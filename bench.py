@@ -1,7 +1,8 @@
 """Benchmark: one decode step of paged GQA decode attention on one MI355X.
 
 A step is one ``sl_decode_attn`` call over the whole synthetic batch (the
-partitioner, the split-KV kernel and the log-sum-exp merge), with every input
+split-KV kernel, which partitions the work itself, and the log-sum-exp
+merge), with every input
 already resident in HBM. Prints one JSON line:
 
   value      algorithmic bytes per step / wall time per step (GB/s), where the

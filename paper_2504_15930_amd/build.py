@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIBRARY = os.path.join(HERE, "libsl.so")
-SOURCES = ["partition.hip", "decode_split.hip", "decode_shared.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
+SOURCES = ["decode_split.hip", "decode_shared.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
            "engine.cpp", "dispatch.cpp"]
 ARCH = "gfx950"
 

@@ -1,7 +1,7 @@
 // Host side of libsl: argument checks, workspace layout, launch geometry and
-// the launches of one decode-attention call (split-KV with its own work
-// partition -> merge; prefix sharing: partition -> fused split -> merge), all
-// enqueued on the caller's stream with no host synchronisation.
+// the launches of one decode-attention call (split-KV, which partitions the
+// work itself -> merge; prefix sharing: fused own- and shared-page split ->
+// merge), all enqueued on the caller's stream with no host synchronisation.
 #include <mutex>
 
 #include "../../include/sl.h"
@@ -45,9 +45,6 @@ size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv
     w.cum_own = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
     w.seq_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4 * (size_t)batch));
     w.cum_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)num_groups + 1)));
-    w.own_tiles = reinterpret_cast<TileEntry *>(take(sizeof(TileEntry) * (size_t)batch * max_blocks * num_kv_heads));
-    w.shared_tiles =
-        reinterpret_cast<TileEntry *>(take(sizeof(TileEntry) * (size_t)num_groups * max_blocks * num_kv_heads));
     w.own_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
     w.own_acc = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
     w.shared_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * kPrefixRows * 2));
@@ -187,16 +184,14 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
         (reinterpret_cast<uintptr_t>(d->workspace) & (kAlign - 1)) != 0)
         return SL_ERR_WORKSPACE;
 
-    // The split kernel partitions the work itself (direct mode): each
-    // workgroup scans the lengths into LDS and walks the block table.
+    // The split kernel partitions the work itself: each workgroup scans the
+    // lengths into LDS and walks the block table.
     SplitParams sp;
     sp.q = q;
     sp.k_pages = k_pages;
     sp.v_pages = v_pages;
     sp.k_scales = k_scales;
     sp.v_scales = v_scales;
-    sp.tiles = nullptr;   // direct mode
-    sp.cum_pages = ws.cum_pages;
     sp.out = out;
     sp.part_ml = ws.part_ml;
     sp.part_acc = ws.part_acc;
@@ -316,24 +311,15 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     const int32_t *gs = num_groups > 0 ? group_start : ws.cum_shared;
     const int32_t *sp = num_groups > 0 ? shared_pages : ws.cum_shared;
 
-    PrefixPartitionParams pp;
-    pp.seq_lens = seq_lens;
-    pp.block_table = block_table;
+    // Both page streams are derived inside the fused split kernel, whose
+    // workgroup 0 stores the sums the merge reads.
+    PrefixParams pp;
     pp.group_start = gs;
     pp.shared_pages = sp;
     pp.cum_own = ws.cum_own;
     pp.cum_shared = ws.cum_shared;
     pp.seq_shared = ws.seq_shared;
-    pp.own_tiles = ws.own_tiles;
-    pp.shared_tiles = ws.shared_tiles;
-    pp.batch = d->batch;
     pp.num_groups = num_groups;
-    pp.num_q_heads = d->num_q_heads;
-    pp.num_kv_heads = d->num_kv_heads;
-    pp.max_blocks = d->max_blocks_per_seq;
-    pp.num_pages = d->num_pages;
-    if (launch_partition_prefix(pp, d->stream) != hipSuccess)
-        return SL_ERR_HIP;
 
     SplitParams sp_;
     sp_.q = q;
@@ -342,6 +328,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.k_scales = nullptr;
     sp_.v_scales = nullptr;
     sp_.out = out;
+    sp_.batch = d->batch;
     sp_.num_kv_heads = d->num_kv_heads;
     sp_.group = G;
     sp_.num_workers = nw;
@@ -349,32 +336,26 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.scale_log2 = scale * 1.4426950408889634f;
     sp_.seq_lens = seq_lens;
     sp_.block_table = block_table;
-    sp_.cum_out = nullptr;   // tile-list mode
+    sp_.cum_out = nullptr;   // the sums go through pp
     sp_.max_blocks = d->max_blocks_per_seq;
     sp_.num_pages = d->num_pages;
     // Shared-page pass: one workgroup of four wavefronts per worker.
     const int nws = shared_workers(nw);
     SplitParams shp = sp_;
     shp.num_workers = nws;
-    shp.tiles = ws.shared_tiles;
-    shp.cum_pages = ws.cum_shared;
-    shp.batch = num_groups;
     shp.part_ml = ws.shared_ml;
     shp.part_acc = ws.shared_acc;
     shp.unit_ml = ws.shared_unit_ml;
     shp.unit_acc = ws.shared_unit_acc;
     // Own-page pass: the single-unit workers.
     sp_.num_workers = nw;
-    sp_.tiles = ws.own_tiles;
-    sp_.cum_pages = ws.cum_own;
-    sp_.batch = d->batch;
     sp_.part_ml = ws.own_ml;
     sp_.part_acc = ws.own_acc;
     sp_.unit_ml = ws.own_unit_ml;
     sp_.unit_acc = ws.own_unit_acc;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
-    if (launch_prefix_split(sp_, shp, d->head_dim, d->stream) != hipSuccess)
+    if (launch_prefix_split(sp_, shp, pp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
         return SL_ERR_HIP;

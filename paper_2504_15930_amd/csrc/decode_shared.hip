@@ -255,11 +255,23 @@ __device__ __forceinline__ void load_q(bf16x8_t (&qop)[D / 32], const SplitParam
             bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(qr, rel * D * 2 + 2 * (32 * s + 8 * quad), 0, 0));
 }
 
-// Worker w (one workgroup) of the shared-page pass.
+// LDS view of the shared-page stream: the exclusive prefix sum of shared
+// pages per group, and each group's first member and size packed as
+// lead | (members - 1) << 16 (a group without shared pages has no tiles).
+struct SharedLds {
+    const int32_t *sh;   // [NG + 1]
+    const int32_t *gl;   // [NG]
+    int32_t num_groups;
+};
+
+// Worker w (one workgroup) of the shared-page pass over the stream that `sv`
+// describes (complete in LDS). Stream tile s = Hkv sh[k] + g s_k + j is page j
+// of group k's shared pages (s_k of them, read through the group's first
+// member's block-table row) for KV head g.
 template <int D>
-__device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w)
+__device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w, const SharedLds &sv)
 {
-    const long long total = (long long)p.cum_pages[p.batch] * p.num_kv_heads;
+    const long long total = (long long)sv.sh[sv.num_groups] * p.num_kv_heads;
     const int nw = effective_workers(total, p.num_workers);
     if (w >= nw)
         return;
@@ -276,18 +288,57 @@ __device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w)
 
     __shared__ __attribute__((aligned(16))) uint8_t stage[2][2 * Geo<D>::kTile];
 
-    // Tile-list entries, read through a bounds-checked buffer resource (an
-    // index past the range is clamped to the last tile); every lane loads the
-    // same entry.
-    const __amdgpu_buffer_rsrc_t ents = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<TileEntry *>(p.tiles + s0), 0, ntiles * (int)sizeof(TileEntry), kRawBufferWord3);
-    auto entry = [&](int i) -> u32x2_t {
-        const int j = i < ntiles ? i : ntiles - 1;
-        return __builtin_bit_cast(
-            u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
+    // Tile entries {block-table entry, metadata, KV head}, fetched in tile
+    // order (every call asks for the next tile; past the range the last tile
+    // repeats) from a cursor (k, g, j) over the stream; the block-table entry
+    // is loaded through a bounds-checked buffer resource, by every lane.
+    const __amdgpu_buffer_rsrc_t btab = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(p.block_table), 0, p.batch * p.max_blocks * (int)sizeof(int32_t), kRawBufferWord3);
+    // Largest k with Hkv sh[k] <= s0 (then group k has shared pages).
+    int klo = 0, khi = sv.num_groups;
+    while (khi - klo > 1) {
+        const int mid = (klo + khi) >> 1;
+        if ((long long)sv.sh[mid] * p.num_kv_heads <= s0)
+            klo = mid;
+        else
+            khi = mid;
+    }
+    int ck = klo;
+    int csk = sv.sh[ck + 1] - sv.sh[ck];
+    int cgl = sv.gl[ck];
+    const int off = (int)(s0 - (long long)sv.sh[ck] * p.num_kv_heads);
+    int cg = off / csk;
+    int cj = off - cg * csk;
+    auto entry = [&](int i) -> u32x4_t {
+        const int lead = cgl & 0xffff;
+        const uint32_t bt = __builtin_bit_cast(
+            uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (lead * p.max_blocks + cj) * 4, 0));
+        uint32_t meta = (uint32_t)(cgl >> 16) | ((uint32_t)(lead * p.num_q_heads + cg * G) << kMetaRowShift);
+        if (cj == 0)
+            meta |= kMetaFirst;
+        if (cj == csk - 1)
+            meta |= kMetaLast;
+        const u32x4_t e = {bt, meta, (uint32_t)cg, 0u};
+        if (i < ntiles - 1) {   // advance to the next tile of the stream
+            if (++cj == csk) {
+                cj = 0;
+                if (++cg == p.num_kv_heads) {
+                    cg = 0;
+                    do
+                        ++ck;
+                    while (sv.sh[ck + 1] == sv.sh[ck]);   // tiles remain, so a group with tiles follows
+                    csk = sv.sh[ck + 1] - sv.sh[ck];
+                    cgl = sv.gl[ck];
+                }
+            }
+        }
+        return e;
     };
-    auto page_of = [](u32x2_t e) { return (int32_t)__builtin_amdgcn_readfirstlane(e[0]); };
-    auto meta_of = [](u32x2_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
+    auto page_of = [&](u32x4_t e) -> int32_t {
+        const uint32_t bt = (uint32_t)__builtin_amdgcn_readfirstlane(e[0]);
+        return bt < (uint32_t)p.num_pages ? (int32_t)(bt * (uint32_t)p.num_kv_heads + e[2]) : -1;
+    };
+    auto meta_of = [](u32x4_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
 
     // Every iteration issues the same loads: tile i + R (its K/V quarters and,
     // when it starts a unit, the unit's query block; empty loads otherwise)
@@ -296,7 +347,7 @@ __device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w)
     // to issue next. The prologue fetches the first 2R entries and waits once.
     constexpr int R = kAhead + 1;
     static_assert(R % 2 == 0, "a ring turn must cover whole stage pairs");
-    u32x2_t first_e[R], ering[R];
+    u32x4_t first_e[R], ering[R];
 #pragma unroll
     for (int k = 0; k < R; ++k)
         first_e[k] = entry(k);
@@ -372,34 +423,102 @@ __device__ __forceinline__ void split_shared_worker(const SplitParams &p, int w)
     }
 }
 
+// Prologue of the fused prefix kernel, run by the whole workgroup: builds in
+// LDS the group of every sequence (-1: none), the lengths, the exclusive
+// prefix sums of own pages per sequence and of shared pages per group, and
+// each group's packed first member and size; workgroup 0 also stores the sums
+// and every sequence's sharing descriptor for the merge. A group that is
+// empty, has more than min(16, kPrefixRows / G) members, or whose range or
+// page count is out of bounds gets no shared pages: its members are attended
+// like unshared sequences, so the result stays exact, only without the saving.
+__device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const PrefixParams &pp, int32_t *s_own,
+                                                   int32_t *s_len, int32_t *s_group, int32_t *s_sh, int32_t *s_gl)
+{
+    constexpr int T = kWave * kWavesPerBlock;
+    const int B = p.batch, NG = pp.num_groups;
+    const int tid = threadIdx.x;
+    const int max_members = min(16, kPrefixRows / p.group);
+    for (int b = tid; b < B; b += T)
+        s_group[b] = -1;
+    __syncthreads();
+    for (int k = tid; k < NG; k += T) {
+        const int lo = pp.group_start[k], hi = pp.group_start[k + 1];
+        const int sp = pp.shared_pages[k];
+        const bool ok = lo >= 0 && hi <= B && hi - lo >= 1 && hi - lo <= max_members && sp > 0 &&
+                        sp <= p.max_blocks;
+        s_sh[k] = ok ? sp : 0;
+        s_gl[k] = ok ? lo | (hi - lo - 1) << 16 : 0;
+        if (ok)
+            for (int b = lo; b < hi; ++b)
+                atomicMax(&s_group[b], k);   // ascending groups never overlap; otherwise every workgroup agrees
+    }
+    __syncthreads();
+    const int max_len = p.max_blocks * kPageSize;
+    for (int b = tid; b < B; b += T) {
+        const int L = p.seq_lens[b];
+        const int k = s_group[b];
+        const int n = pages_of(L, max_len);
+        const int sh = k >= 0 ? s_sh[k] : 0;
+        s_len[b] = L;
+        s_own[b] = n > sh ? n - sh : 0;
+    }
+    __syncthreads();
+    block_exclusive_scan(s_own, B);
+    block_exclusive_scan(s_sh, NG);
+    if (blockIdx.x == 0) {
+        for (int i = tid; i <= B; i += T)
+            pp.cum_own[i] = s_own[i];
+        for (int i = tid; i <= NG; i += T)
+            pp.cum_shared[i] = s_sh[i];
+        typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+        for (int i = tid; i < B; i += T) {
+            const int k = s_group[i];
+            *reinterpret_cast<i32x4_t *>(pp.seq_shared + 4 * (size_t)i) =
+                k >= 0 ? i32x4_t{s_sh[k], s_sh[k + 1] - s_sh[k], s_gl[k] & 0xffff, k} : i32x4_t{0, 0, 0, -1};
+        }
+    }
+}
+
 // Both passes of prefix-shared attention in one launch: workgroups
 // [0, own_blocks) run the single-unit workers of the own pages (four per
 // workgroup), the rest run shared-page workers. The own-page workgroups come
 // first, so each CU holds one of them beside a shared-page workgroup: the
 // memory-bound and the MFMA-heavy pass share the CUs instead of running one
-// after the other.
+// after the other. Every workgroup first derives both streams in its dynamic
+// LDS (3 B + 2 NG + 2 ints).
 template <int D>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(SplitParams own, SplitParams shared,
-                                                                               int own_blocks)
+                                                                               PrefixParams pp, int own_blocks)
 {
+    extern __shared__ int32_t s_dyn[];
+    const int B = own.batch, NG = pp.num_groups;
+    int32_t *const s_own = s_dyn;            // [B + 1]
+    int32_t *const s_len = s_own + B + 1;    // [B]
+    int32_t *const s_group = s_len + B;      // [B]
+    int32_t *const s_sh = s_group + B;       // [NG + 1]
+    int32_t *const s_gl = s_sh + NG + 1;     // [NG]
+    scan_prefix_groups(own, pp, s_own, s_len, s_group, s_sh, s_gl);
     if ((int)blockIdx.x < own_blocks)
-        split_unit_worker<D, false, false>(
-            own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), nullptr);
+        split_unit_worker<D, false, kOwnPages>(
+            own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+            StreamLds{s_own, s_len, s_group, s_sh});
     else
-        split_shared_worker<D>(shared, (int)blockIdx.x - own_blocks);
+        split_shared_worker<D>(shared, (int)blockIdx.x - own_blocks, SharedLds{s_sh, s_gl, NG});
 }
 
 }  // namespace
 
-hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int head_dim, hipStream_t stream)
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, const PrefixParams &pp,
+                               int head_dim, hipStream_t stream)
 {
     const int own_blocks = (own.num_workers + kWavesPerBlock - 1) / kWavesPerBlock;
     const dim3 grid(own_blocks + shared.num_workers);
     const dim3 block(kWave * kWavesPerBlock);
+    const size_t lds = prefix_dynamic_lds(own.batch, pp.num_groups);
     if (head_dim == 128)
-        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, 0, stream, own, shared, own_blocks);
+        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, lds, stream, own, shared, pp, own_blocks);
     else if (head_dim == 64)
-        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, 0, stream, own, shared, own_blocks);
+        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, lds, stream, own, shared, pp, own_blocks);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

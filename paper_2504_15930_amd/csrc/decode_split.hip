@@ -6,14 +6,17 @@
 namespace sl {
 namespace {
 
-// Direct mode: every workgroup derives the tile stream from the lengths and
-// the block table (its dynamic LDS holds the page prefix sum and the lengths).
+// Every workgroup derives the tile stream from the lengths and the block
+// table (its dynamic LDS holds the page prefix sum and the lengths).
 template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
     extern __shared__ int32_t s_dyn[];
-    split_unit_worker<D, FP8, true>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
-                                    s_dyn);
+    int32_t *const s_cum = s_dyn;              // [B + 1]
+    int32_t *const s_len = s_dyn + p.batch + 1;  // [B]
+    scan_sequences(p, s_cum, s_len);
+    split_unit_worker<D, FP8, kAllPages>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+                                         StreamLds{s_cum, s_len, nullptr, nullptr});
 }
 
 }  // namespace

@@ -122,7 +122,7 @@ struct Tile {
     uint32_t v[VW];
     u32x4_t q[D / 32];   // the unit's query rows, loaded with a unit's first tile only
     float scl;           // FP8: key scale in lanes 0-31, value scale in lanes 32-63
-    uint32_t meta;       // TileEntry::meta (wave-uniform)
+    uint32_t meta;       // tile metadata (kMeta* bits, wave-uniform)
     bool bad_page;       // the block table named a page outside the pool
 };
 
@@ -393,27 +393,19 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
     }
 }
 
-// Direct mode, run by the whole workgroup before its workers start: the
-// pages per sequence n_b = ceil(clamp(L_b, 0, max_blocks * 16) / 16), their
-// exclusive prefix sum in s_cum[0 .. B] and the lengths in s_len[0 .. B), all
-// in LDS; workgroup 0 also stores the prefix sum for the merge.
-__device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_cum, int32_t *s_len)
+// Turns a[0, n) (in LDS, written before a barrier) into its exclusive
+// prefix sum and stores the total in a[n]. Every thread of the workgroup
+// calls it; each scans a contiguous run. Ends with a barrier.
+__device__ __forceinline__ void block_exclusive_scan(int32_t *a, int n)
 {
     __shared__ int32_t s_wave[kWavesPerBlock];
     constexpr int T = kWave * kWavesPerBlock;
-    const int B = p.batch;
     const int tid = threadIdx.x;
-    const int max_len = p.max_blocks * kPageSize;
-    const int per = (B + T - 1) / T;
-    const int lo = min(B, tid * per), hi = min(B, lo + per);
+    const int per = (n + T - 1) / T;
+    const int lo = min(n, tid * per), hi = min(n, lo + per);
     int local = 0;
-    for (int b = lo; b < hi; ++b) {
-        const int L = p.seq_lens[b];
-        const int nb = L <= 0 ? 0 : (min(L, max_len) + kPageSize - 1) / kPageSize;
-        s_len[b] = L;
-        s_cum[b] = nb;
-        local += nb;
-    }
+    for (int i = lo; i < hi; ++i)
+        local += a[i];
     const int lane = tid & (kWave - 1), wave = tid / kWave;
     int incl = local;
 #pragma unroll
@@ -432,32 +424,66 @@ __device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_
         total += s_wave[k];
     }
     int run = base + incl - local;
-    for (int b = lo; b < hi; ++b) {
-        const int nb = s_cum[b];
-        s_cum[b] = run;
-        run += nb;
+    for (int i = lo; i < hi; ++i) {
+        const int v = a[i];
+        a[i] = run;
+        run += v;
     }
     if (tid == 0)
-        s_cum[B] = total;
+        a[n] = total;
     __syncthreads();
+}
+
+// Pages of a sequence of length L: ceil(clamp(L, 0, max_len) / 16).
+__device__ __forceinline__ int pages_of(int L, int max_len)
+{
+    return L <= 0 ? 0 : (min(L, max_len) + kPageSize - 1) / kPageSize;
+}
+
+// Plain attention, run by the whole workgroup before its workers start: the
+// pages per sequence, their exclusive prefix sum in s_cum[0 .. B] and the
+// lengths in s_len[0 .. B), all in LDS; workgroup 0 also stores the prefix sum
+// for the merge.
+__device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_cum, int32_t *s_len)
+{
+    constexpr int T = kWave * kWavesPerBlock;
+    const int B = p.batch;
+    const int max_len = p.max_blocks * kPageSize;
+    for (int b = threadIdx.x; b < B; b += T) {
+        const int L = p.seq_lens[b];
+        s_len[b] = L;
+        s_cum[b] = pages_of(L, max_len);
+    }
+    __syncthreads();
+    block_exclusive_scan(s_cum, B);
     if (blockIdx.x == 0)
-        for (int b = tid; b <= B; b += T)
+        for (int b = threadIdx.x; b <= B; b += T)
             p.cum_out[b] = s_cum[b];
 }
 
-// Worker w (one wavefront) of the single-unit split-KV pass. With DIRECT the
-// tiles come from the lengths and the block table (s_dyn: 2 B + 1 ints of
-// LDS, and the whole workgroup must call this); otherwise from the tile list.
-template <int D, bool FP8, bool DIRECT>
-__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, int32_t *s_dyn)
+// Which tiles a single-unit worker streams.
+constexpr int kAllPages = 0;   // plain attention: every page of every sequence
+constexpr int kOwnPages = 1;   // prefix sharing: the pages after each sequence's shared ones
+
+// LDS view of the unit stream: the exclusive prefix sum of tiles per sequence
+// and the lengths; for kOwnPages also each sequence's group and the groups'
+// shared-page prefix sum (a sequence's own pages start after its group's
+// shared pages).
+struct StreamLds {
+    const int32_t *cum;     // [B + 1]
+    const int32_t *len;     // [B]
+    const int32_t *group;   // [B], kOwnPages only (-1: no shared pages)
+    const int32_t *sh;      // [NG + 1], kOwnPages only
+};
+
+// Worker w (one wavefront) of the single-unit split-KV pass over the stream
+// that `sv` describes (in LDS, complete: the caller has passed a barrier).
+template <int D, bool FP8, int MODE>
+__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, const StreamLds &sv)
 {
-    int32_t *const s_cum = s_dyn;
-    int32_t *const s_len = s_dyn + p.batch + 1;
-    if constexpr (DIRECT)
-        scan_sequences(p, s_cum, s_len);
     if (w >= p.num_workers)
         return;
-    const long long total = (long long)(DIRECT ? s_cum[p.batch] : p.cum_pages[p.batch]) * p.num_kv_heads;
+    const long long total = (long long)sv.cum[p.batch] * p.num_kv_heads;
     const int nw = effective_workers(total, p.num_workers);
     if (w >= nw)
         return;
@@ -475,77 +501,73 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, i
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 
     // Tile entries, fetched in tile order (every call below asks for the next
-    // tile; past the range the last tile repeats). An entry is {page-head tile
-    // index, or -1 for a page outside the pool; metadata}, read from the tile
-    // list through a bounds-checked buffer resource, or in direct mode {block-
-    // table entry (loaded), metadata and KV head (from a cursor over the
-    // units)}.
-    const __amdgpu_buffer_rsrc_t ents = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<TileEntry *>(p.tiles + s0), 0, ntiles * (int)sizeof(TileEntry), kRawBufferWord3);
+    // tile; past the range the last tile repeats): {block-table entry (loaded
+    // through a bounds-checked buffer resource), metadata, KV head}, from a
+    // cursor over the units.
     const __amdgpu_buffer_rsrc_t btab = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int32_t *>(p.block_table), 0, p.batch * p.max_blocks * (int)sizeof(int32_t), kRawBufferWord3);
-    // Direct-mode cursor: tile (b, g, j) of the stream, n_b and L_b.
-    int cb = 0, cg = 0, cj = 0, cnb = 0, clen = 0;
-    if constexpr (DIRECT) {
-        // Largest b with Hkv cum[b] <= s0 (then its n_b > 0).
-        int blo = 0, bhi = p.batch;
-        while (bhi - blo > 1) {
-            const int mid = (blo + bhi) >> 1;
-            if ((long long)s_cum[mid] * p.num_kv_heads <= s0)
-                blo = mid;
-            else
-                bhi = mid;
-        }
-        cb = blo;
-        cnb = s_cum[cb + 1] - s_cum[cb];
-        clen = s_len[cb];
-        const int off = (int)(s0 - (long long)s_cum[cb] * p.num_kv_heads);
-        cg = off / cnb;
-        cj = off - cg * cnb;
-    }
-    const int max_len = p.max_blocks * kPageSize;
-    auto entry = [&](int i) -> u32x4_t {
-        if constexpr (!DIRECT) {
-            const int j = i < ntiles ? i : ntiles - 1;
-            const u32x2_t e = __builtin_bit_cast(
-                u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(ents, 0, j * (int)sizeof(TileEntry), 0));
-            return u32x4_t{e[0], e[1], 0u, 0u};
+    // Cursor: tile (b, g, j) of the stream, the sequence's tile count n_b and
+    // length L_b, and the page index its tiles start at (its group's shared
+    // pages for kOwnPages, else 0).
+    auto shared_of = [&](int b) -> int {
+        if constexpr (MODE == kOwnPages) {
+            const int k = sv.group[b];
+            return k >= 0 ? sv.sh[k + 1] - sv.sh[k] : 0;
         } else {
-            const uint32_t bt = __builtin_bit_cast(
-                uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (cb * p.max_blocks + cj) * 4, 0));
-            const int live = min(kPageSize, clen - cj * kPageSize);
-            uint32_t meta = (uint32_t)(max(live, 1) - 1) |
-                            ((uint32_t)(cb * p.num_q_heads + cg * G) << kMetaRowShift);
-            if (cj == 0)
-                meta |= kMetaFirst;
-            if (cj == cnb - 1)
-                meta |= kMetaLast;
-            if (clen > max_len)
-                meta |= kMetaBadLen;
-            const u32x4_t e = {bt, meta, (uint32_t)cg, 0u};
-            if (i < ntiles - 1) {   // advance to the next tile of the stream
-                if (++cj == cnb) {
-                    cj = 0;
-                    if (++cg == p.num_kv_heads) {
-                        cg = 0;
-                        do
-                            ++cb;
-                        while (s_cum[cb + 1] == s_cum[cb]);   // tiles remain, so a sequence with pages follows
-                        cnb = s_cum[cb + 1] - s_cum[cb];
-                        clen = s_len[cb];
-                    }
-                }
-            }
-            return e;
+            return 0;
         }
     };
-    auto page_of = [&](u32x4_t e) -> int32_t {
-        if constexpr (!DIRECT) {
-            return (int32_t)__builtin_amdgcn_readfirstlane(e[0]);
-        } else {
-            const uint32_t bt = (uint32_t)__builtin_amdgcn_readfirstlane(e[0]);
-            return bt < (uint32_t)p.num_pages ? (int32_t)(bt * (uint32_t)p.num_kv_heads + e[2]) : -1;
+    // Largest b with Hkv cum[b] <= s0 (then its n_b > 0).
+    int blo = 0, bhi = p.batch;
+    while (bhi - blo > 1) {
+        const int mid = (blo + bhi) >> 1;
+        if ((long long)sv.cum[mid] * p.num_kv_heads <= s0)
+            blo = mid;
+        else
+            bhi = mid;
+    }
+    int cb = blo;
+    int cnb = sv.cum[cb + 1] - sv.cum[cb];
+    int clen = sv.len[cb];
+    int csh = shared_of(cb);
+    const int off = (int)(s0 - (long long)sv.cum[cb] * p.num_kv_heads);
+    int cg = off / cnb;
+    int cj = off - cg * cnb;
+    const int max_len = p.max_blocks * kPageSize;
+    auto entry = [&](int i) -> u32x4_t {
+        const int pg = csh + cj;   // page index in the sequence
+        const uint32_t bt = __builtin_bit_cast(
+            uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (cb * p.max_blocks + pg) * 4, 0));
+        const int live = min(kPageSize, clen - pg * kPageSize);
+        uint32_t meta = (uint32_t)(max(live, 1) - 1) | ((uint32_t)(cb * p.num_q_heads + cg * G) << kMetaRowShift);
+        if (cj == 0)
+            meta |= kMetaFirst;
+        if (cj == cnb - 1)
+            meta |= kMetaLast;
+        if (clen > max_len)
+            meta |= kMetaBadLen;
+        if (csh > 0)
+            meta |= kMetaPrefixed;
+        const u32x4_t e = {bt, meta, (uint32_t)cg, 0u};
+        if (i < ntiles - 1) {   // advance to the next tile of the stream
+            if (++cj == cnb) {
+                cj = 0;
+                if (++cg == p.num_kv_heads) {
+                    cg = 0;
+                    do
+                        ++cb;
+                    while (sv.cum[cb + 1] == sv.cum[cb]);   // tiles remain, so a sequence with tiles follows
+                    cnb = sv.cum[cb + 1] - sv.cum[cb];
+                    clen = sv.len[cb];
+                    csh = shared_of(cb);
+                }
+            }
         }
+        return e;
+    };
+    auto page_of = [&](u32x4_t e) -> int32_t {
+        const uint32_t bt = (uint32_t)__builtin_amdgcn_readfirstlane(e[0]);
+        return bt < (uint32_t)p.num_pages ? (int32_t)(bt * (uint32_t)p.num_kv_heads + e[2]) : -1;
     };
     auto meta_of = [](u32x4_t e) { return (uint32_t)__builtin_amdgcn_readfirstlane(e[1]); };
 

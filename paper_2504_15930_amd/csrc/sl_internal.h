@@ -1,6 +1,6 @@
 // Internal interface between the host-side entry points (api.cpp) and the
 // gfx950 kernels (decode_split.hip with the worker in decode_unit.h,
-// decode_shared.hip, partition.hip, merge.hip, append.hip, engine.hip), and
+// decode_shared.hip, merge.hip, append.hip, engine.hip), and
 // the decode engine (engine.cpp).
 //
 // Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
@@ -13,14 +13,13 @@
 // chip idle (the on-chip analogue of StreamRL's skewness bubbles, Section 2.4
 // and Section 5.1).
 //
-// A worker streams its range as one flat sequence of tiles. In plain decode
-// attention each workgroup derives the stream itself: it scans the lengths
-// into LDS, locates its workers' first tiles by binary search and walks the
-// block table with a cursor (direct mode). Prefix-shared attention streams
-// tile lists of one 8-byte entry per tile (TileEntry), written by its
-// partitioner. Either way the entry of a tile is fetched a pipeline turn
-// ahead, so unit boundaries inside the range cost no dependent load and do
-// not drain the load pipeline.
+// A worker streams its range as one flat sequence of tiles, which every
+// workgroup derives itself: it scans the lengths (and, with prefix sharing,
+// the group descriptions) into LDS, locates its workers' first tiles by
+// binary search and walks the block table with a cursor. There is no
+// partitioning launch and no tile list in memory. The block-table entry of a
+// tile is fetched a pipeline turn ahead, so unit boundaries inside the range
+// cost no dependent load and do not drain the load pipeline.
 //
 // A unit that lies inside one worker's range is finished by that worker; a
 // unit cut by a range boundary leaves one partial softmax state per worker
@@ -41,7 +40,6 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;          // split kernel: 4 independent workers per block
 constexpr int kMaxGroup = 16;              // query heads per KV head (one MFMA column block)
 constexpr int kMaxBatch = 8192;            // the split kernel keeps two ints per sequence in LDS
-constexpr int kPartitionThreads = 1024;
 constexpr int kMergeThreads = 256;         // one wave per unit, four units per block
 constexpr int kMaxWorkers = 1 << 16;       // keeps partial-state offsets below 2^31 bytes
 #ifndef SL_MIN_TILES_PER_WORKER
@@ -61,22 +59,18 @@ __host__ __device__ inline int effective_workers(long long total, int num_worker
 }
 constexpr size_t kAlign = 256;
 
-// Tile entry. `page` = page_id * Hkv + g, the index of the tile in the
-// [num_pages][Hkv] grid of page-head tiles (-1: the block table named a page
-// outside the pool). `meta` packs, from bit 0:
+// Tile metadata, one wave-uniform word per tile, from bit 0:
 //   [3:0] live tokens in the tile minus one, [4] last tile of its unit,
 //   [5] first tile of its unit, [6] the sequence length is invalid,
-//   [31:8] first query row of the unit, b * Hq + g * G.
-struct TileEntry {
-    int32_t page;
-    uint32_t meta;
-};
+//   [7] see kMetaPrefixed, [31:8] first query row of the unit, b * Hq + g * G.
+// A tile's KV data is page-head tile page_id * Hkv + g of the
+// [num_pages][Hkv] grid (-1: the block table named a page outside the pool).
 constexpr uint32_t kMetaLast = 1u << 4;
 constexpr uint32_t kMetaFirst = 1u << 5;
 constexpr uint32_t kMetaBadLen = 1u << 6;
 constexpr uint32_t kMetaPrefixed = 1u << 7;   // own-page unit of a sequence whose first pages are shared
-// Prefix-sharing mode: a shared-prefix tile list holds, per (group, KV head),
-// the group's shared pages once; its entries keep members - 1 in bits [3:0]
+// Prefix-sharing mode: the shared-page stream holds, per (group, KV head),
+// the group's shared pages once; their metadata keeps members - 1 in bits [3:0]
 // (every shared page is full) and the first query row of the group's first
 // member in [31:8]. The query rows of a shared unit are (member j, head h) ->
 // row0 + j * Hq + h, at most kPrefixRows of them (kPrefixBlocks MFMA column
@@ -97,8 +91,6 @@ struct SplitParams {
     const void *v_pages;
     const float *k_scales;
     const float *v_scales;
-    const TileEntry *tiles;
-    const int32_t *cum_pages;
     uint16_t *out;
     float *part_ml;
     float *part_acc;
@@ -111,9 +103,9 @@ struct SplitParams {
     // row stride of part_ml / part_acc; null otherwise.
     float *unit_ml;
     float *unit_acc;
-    // Direct mode (no tile list): the kernel derives every tile from the
-    // lengths and the block table itself, and workgroup 0 stores the page
-    // prefix sum in cum_out for the merge.
+    // The kernel derives every tile from the lengths and the block table
+    // itself; workgroup 0 stores the page prefix sum in cum_out for the merge
+    // (plain attention; prefix sharing stores its sums through PrefixParams).
     const int32_t *seq_lens;
     const int32_t *block_table;
     int32_t *cum_out;
@@ -122,19 +114,17 @@ struct SplitParams {
 
 // Prefix-sharing mode. Groups are runs of consecutive sequences
 // [group_start[k], group_start[k+1]) whose first shared_pages[k] block-table
-// entries are the same; the group's first member's entries are used.
-struct PrefixPartitionParams {
-    const int32_t *seq_lens;
-    const int32_t *block_table;
+// entries are the same; the group's first member's entries are used. Every
+// workgroup of the fused split kernel derives both page streams from these;
+// workgroup 0 stores the sums below for the merge.
+struct PrefixParams {
     const int32_t *group_start;   // [num_groups + 1]
     const int32_t *shared_pages;  // [num_groups]
     int32_t *cum_own;             // [B + 1] prefix sum of own (unshared) pages
     int32_t *cum_shared;          // [num_groups + 1] prefix sum of shared pages
     int32_t *seq_shared;          // [B][4] per sequence: first shared page of its group in the shared
                                   // stream, shared pages, group's first member, group (-1, zeros if unshared)
-    TileEntry *own_tiles;         // [B * max_blocks * Hkv]
-    TileEntry *shared_tiles;      // [num_groups * max_blocks * Hkv]
-    int32_t batch, num_groups, num_q_heads, num_kv_heads, max_blocks, num_pages;
+    int32_t num_groups;
 };
 
 struct PrefixMergeParams {
@@ -143,7 +133,7 @@ struct PrefixMergeParams {
     const int32_t *shared_pages;
     const int32_t *cum_own;
     const int32_t *cum_shared;
-    const int32_t *seq_shared;   // [B][4], as written by the partitioner
+    const int32_t *seq_shared;   // [B][4], as written by the split kernel
     const float *own_ml, *own_acc;        // [2 NW][G][2], [2 NW][G][D]
     const float *shared_ml, *shared_acc;  // [2 NW][kPrefixRows][2], [2 NW][kPrefixRows][D]
     const float *own_unit_ml, *own_unit_acc;        // [B Hkv][G][2 | D]: whole own units
@@ -174,11 +164,10 @@ struct AppendParams {
     int32_t batch, num_kv_heads, max_blocks, num_pages;
 };
 
-constexpr int kMaxPrefixBatch = 4096;      // the prefix partitioner keeps three ints per sequence in LDS
+constexpr int kMaxPrefixBatch = 4096;      // the fused prefix kernel keeps three ints per sequence in LDS
 
 struct PrefixWorkspace {
     int32_t *cum_own, *seq_shared, *cum_shared;
-    TileEntry *own_tiles, *shared_tiles;
     float *own_ml, *own_acc, *shared_ml, *shared_acc;
     float *own_unit_ml, *own_unit_acc, *shared_unit_ml, *shared_unit_acc;
 };
@@ -189,16 +178,23 @@ size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv
 size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads, int group,
                         int head_dim, int num_workers, Workspace *ws);
 
-// The direct-mode split kernel's dynamic LDS: the page prefix sum (B + 1
-// ints) and the lengths (B ints).
+// The split kernel's dynamic LDS: the page prefix sum (B + 1 ints) and the
+// lengths (B ints).
 inline size_t split_dynamic_lds(int batch) { return sizeof(int32_t) * (2 * (size_t)batch + 1); }
+// The fused prefix kernel's: for the sequences the own-page prefix sum, the
+// lengths and the groups (3 B + 1 ints), for the groups the shared-page prefix
+// sum and the packed first member and size (2 NG + 1 ints).
+inline size_t prefix_dynamic_lds(int batch, int num_groups)
+{
+    return sizeof(int32_t) * (3 * (size_t)batch + 2 * (size_t)num_groups + 2);
+}
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Prefix mode: the own-page pass (single-unit workers) and the shared-page
 // pass (one workgroup of kPrefixBlocks wavefronts per worker, one 16-row
 // column block each, partial states only; shared.num_workers counts
-// workgroups) in one launch, and the partitioner / merge around them.
-hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int head_dim, hipStream_t stream);
-hipError_t launch_partition_prefix(const PrefixPartitionParams &p, hipStream_t stream);
+// workgroups) in one launch, followed by the merge.
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, const PrefixParams &pp,
+                               int head_dim, hipStream_t stream);
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);

@@ -145,3 +145,17 @@ def test_page_count_beyond_block_table_is_unshared():
     ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
                              case["scale"])
     parity.assert_parity(out, ref, "page count beyond the table")
+
+
+def test_max_prefix_batch_many_groups():
+    """The largest batch prefix sharing accepts (4096 sequences), in 2048 groups of two: every
+    workgroup keeps 3 B + 2 NG + 2 ints of stream description in LDS, and the shared-page
+    stream crosses a group boundary every few tiles. Every row against the oracle."""
+    rng = np.random.default_rng(54)
+    ng = 2048
+    case, starts, shared = grpo_case(rng, [2] * ng, list(rng.integers(16, 49, ng)), 40, 8, 2, 64)
+    assert len(case["seq_lens"]) == 4096
+    out = run_prefix(case, starts, shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "batch 4096, 2048 groups")
