@@ -21,13 +21,14 @@
  * pages on admission and one more page in each step whose new token starts a
  * page; a finished sample's pages return to the stack last block first.
  *
- * Every step, on desc.stream and in this order: the step's sequence lengths
- * and new block-table entries are read by the device from a mapped pinned
- * staging buffer and applied; new
- * prompt pages are filled; sl_kv_append stores the step's new K/V rows (the
- * caller's k_new / v_new buffers, the same every step); sl_decode_attn (or
- * _fp8) computes the step's attention output into `out` with the caller's q.
- * Slots without a sample have length 0 (zero output rows).
+ * Every step, on desc.stream and in this order: new prompt pages are filled;
+ * one KV-append launch stores the step's new K/V rows (the caller's k_new /
+ * v_new buffers, the same every step, with the quantise-on-write of
+ * sl_kv_append_fp8 for an E4M3 cache) and also writes the step's sequence
+ * lengths and new block-table entries into seq_lens and block_table, all read
+ * by the device from a mapped pinned staging buffer; sl_decode_attn (or _fp8)
+ * computes the step's attention output into `out` with the caller's q. Slots
+ * without a sample have length 0 (zero output rows).
  *
  * The schedule is fixed by the lengths given at creation, so the host never
  * waits for the device during a run: steps are enqueued asynchronously, and

@@ -261,6 +261,10 @@ sl_status run_append(const sl_attn_desc *d, const uint16_t *k_new, const uint16_
     ap.num_kv_heads = d->num_kv_heads;
     ap.max_blocks = d->max_blocks_per_seq;
     ap.num_pages = d->num_pages;
+    ap.stage = nullptr;
+    ap.n_upd = 0;
+    ap.set_seq_lens = nullptr;
+    ap.set_block_table = nullptr;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (launch_append(ap, d->head_dim, fp8, d->stream) != hipSuccess)

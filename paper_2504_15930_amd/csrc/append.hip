@@ -140,19 +140,31 @@ __device__ __forceinline__ void append_e4m3(const uint16_t *x, uint8_t *tile, fl
 template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void append_kernel(AppendParams p)
 {
+    if (p.stage) {
+        // The step's bookkeeping, for the launches that follow (nothing in
+        // this launch reads the lengths or the block table from memory in
+        // this mode). Indices were checked by the engine.
+        const int nthreads = gridDim.x * blockDim.x;
+        for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < p.batch; i += nthreads)
+            p.set_seq_lens[i] = p.stage[i];
+        for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < p.n_upd; i += nthreads) {
+            const int32_t *u = p.stage + 2 * p.batch + 3 * i;
+            p.set_block_table[(size_t)u[0] * p.max_blocks + u[1]] = u[2];
+        }
+    }
     const int unit = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (unit >= p.batch * p.num_kv_heads)
         return;
     const int lane = threadIdx.x & (kWave - 1);
     const int b = unit / p.num_kv_heads;
     const int g = unit - b * p.num_kv_heads;
-    const int L = p.seq_lens[b];
+    const int L = p.stage ? p.stage[b] : p.seq_lens[b];
     // Nothing to append for an empty sequence; an invalid length or page id
     // leaves the cache untouched.
     if (L <= 0 || L > p.max_blocks * kPageSize)
         return;
     const int t = L - 1;
-    const int page = p.block_table[(size_t)b * p.max_blocks + t / kPageSize];
+    const int page = p.stage ? p.stage[p.batch + b] : p.block_table[(size_t)b * p.max_blocks + t / kPageSize];
     if (page < 0 || page >= p.num_pages)
         return;
     const int slot = t % kPageSize;

@@ -3,13 +3,14 @@
 // The host owns the schedule. Samples are admitted in LPT (or index) order
 // into BS slots, pages come from a LIFO free stack, and the lengths given at
 // creation fix every step in advance. Each step is packed into a pinned
-// staging buffer ([seq_lens][block-table updates][prompt pages to fill]),
-// followed by four launches on the
-// caller's stream: apply, fill (only when a prompt was admitted), KV append
-// and decode attention. The apply and fill kernels read the staging buffer in
-// place (mapped pinned memory), which saves a copy command per step; a ring of
-// such buffers, each reused only once the kernels that read it have
-// completed, lets the host run ahead of the GPU.
+// staging buffer ([seq_lens][page of each new token][block-table updates]
+// [prompt pages to fill]), followed by the launches on the caller's stream:
+// fill (only when a prompt was admitted), KV append (which also applies the
+// step's lengths and block-table updates) and decode attention. The fill and
+// append kernels read the staging buffer in place (mapped pinned memory),
+// which saves a copy command per step; a ring of such buffers, each reused
+// only once the kernels that read it have completed, lets the host run ahead
+// of the GPU.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -106,6 +107,7 @@ sl_status sl_engine::one_step()
         const int i = occupant[b];
         if (i < 0) {
             h[b] = 0;
+            h[BS + b] = -1;
             continue;
         }
         const int t = prompt[i] + made[b];   // position of this step's token
@@ -116,39 +118,50 @@ sl_status sl_engine::one_step()
             upd.insert(upd.end(), {b, t / kPageSize, pg});
         }
         h[b] = t + 1;
+        h[BS + b] = pages[b][t / kPageSize];
     }
     const int n_upd = (int)upd.size() / 3;
     const int n_fill = (int)fills.size();
-    std::memcpy(h + BS, upd.data(), sizeof(int32_t) * upd.size());
-    std::memcpy(h + BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
+    std::memcpy(h + 2 * BS, upd.data(), sizeof(int32_t) * upd.size());
+    std::memcpy(h + 2 * BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
     hipStream_t s = step_desc.stream;
     const int32_t *ds = d_stage[r];
-    if (sl::launch_engine_apply(ds, BS, n_upd, max_blocks, buf.seq_lens, buf.block_table, s) != hipSuccess)
-        return SL_ERR_HIP;
+    // Prompt data first: the new token of an admitted sample may land in its last prompt page.
     if (n_fill > 0 &&
-        sl::launch_engine_fill(ds + BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
+        sl::launch_engine_fill(ds + 2 * BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
                                buf.k_scales, buf.v_scales, s) != hipSuccess)
+        return SL_ERR_HIP;
+    sl::AppendParams ap;
+    ap.k_new = buf.k_new;
+    ap.v_new = buf.v_new;
+    ap.block_table = nullptr;   // the lengths and token pages come from the staging buffer
+    ap.seq_lens = nullptr;
+    ap.k_pages = buf.k_pages;
+    ap.v_pages = buf.v_pages;
+    ap.k_scales = fp8 ? buf.k_scales : nullptr;
+    ap.v_scales = fp8 ? buf.v_scales : nullptr;
+    ap.batch = BS;
+    ap.num_kv_heads = Hkv;
+    ap.max_blocks = max_blocks;
+    ap.num_pages = num_pages;
+    ap.stage = ds;
+    ap.n_upd = n_upd;
+    ap.set_seq_lens = buf.seq_lens;
+    ap.set_block_table = buf.block_table;
+    if (sl::launch_append(ap, D, fp8, s) != hipSuccess)
         return SL_ERR_HIP;
     if (hipEventRecord(ev[r], s) != hipSuccess)   // the staging buffer is free again after this
         return SL_ERR_HIP;
     ev_pending[r] = true;
     sl_status st;
-    if (fp8) {
-        st = sl_kv_append_fp8(&step_desc, buf.k_new, buf.v_new, buf.block_table, buf.seq_lens,
-                              static_cast<uint8_t *>(buf.k_pages), static_cast<uint8_t *>(buf.v_pages),
-                              buf.k_scales, buf.v_scales);
-        if (st == SL_OK)
-            st = sl_decode_attn_fp8(&step_desc, buf.q, static_cast<const uint8_t *>(buf.k_pages),
-                                    static_cast<const uint8_t *>(buf.v_pages), buf.k_scales, buf.v_scales,
-                                    buf.block_table, buf.seq_lens, attn_scale, buf.out);
-    } else {
-        st = sl_kv_append(&step_desc, buf.k_new, buf.v_new, buf.block_table, buf.seq_lens,
-                          static_cast<uint16_t *>(buf.k_pages), static_cast<uint16_t *>(buf.v_pages));
-        if (st == SL_OK)
-            st = sl_decode_attn(&step_desc, buf.q, static_cast<const uint16_t *>(buf.k_pages),
-                                static_cast<const uint16_t *>(buf.v_pages), buf.block_table, buf.seq_lens,
-                                attn_scale, buf.out);
-    }
+    if (fp8)
+        st = sl_decode_attn_fp8(&step_desc, buf.q, static_cast<const uint8_t *>(buf.k_pages),
+                                static_cast<const uint8_t *>(buf.v_pages), buf.k_scales, buf.v_scales,
+                                buf.block_table, buf.seq_lens, attn_scale, buf.out);
+    else
+        st = sl_decode_attn(&step_desc, buf.q, static_cast<const uint16_t *>(buf.k_pages),
+                            static_cast<const uint16_t *>(buf.v_pages), buf.block_table, buf.seq_lens,
+                            attn_scale, buf.out);
     if (st != SL_OK)
         return st;
 
@@ -245,8 +258,8 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     e->slot.assign(M, -1);
     e->admit.assign(M, -1);
     e->finish.assign(M, -1);
-    // staging: lengths, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
-    e->stage_ints = (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
+    // staging: lengths, token pages, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
+    e->stage_ints = 2 * (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
     bool ok = true;
     for (int r = 0; ok && r < kRing; ++r)
         ok = hipHostMalloc(reinterpret_cast<void **>(&e->h_stage[r]), sizeof(int32_t) * e->stage_ints,

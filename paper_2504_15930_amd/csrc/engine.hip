@@ -1,27 +1,12 @@
-// Device helpers of the decode engine (engine.cpp): applying one step's
-// bookkeeping (sequence lengths, new block-table entries) and filling newly
-// admitted prompts' pages with synthetic key/value data.
+// Device helper of the decode engine (engine.cpp): filling newly admitted
+// prompts' pages with synthetic key/value data. (A step's bookkeeping is
+// applied by the KV-append launch, append.hip.)
 #include "sl_internal.h"
 
 namespace sl {
 namespace {
 
 constexpr int kEngineThreads = 256;
-
-// stage = [seq_lens: bs][updates: n_upd x (slot, block, page)]. Every index was
-// checked on the host (slot < bs, block < max_blocks).
-__global__ __launch_bounds__(kEngineThreads) void engine_apply_kernel(const int32_t *stage, int32_t bs,
-                                                                      int32_t n_upd, int32_t max_blocks,
-                                                                      int32_t *seq_lens, int32_t *block_table)
-{
-    const int i = blockIdx.x * kEngineThreads + threadIdx.x;
-    if (i < bs)
-        seq_lens[i] = stage[i];
-    if (i < n_upd) {
-        const int32_t *u = stage + bs + 3 * i;
-        block_table[(size_t)u[0] * max_blocks + u[1]] = u[2];
-    }
-}
 
 // 32-bit integer mixer ("lowbias32": xorshift-multiply rounds).
 __device__ __forceinline__ uint32_t mix32(uint32_t x)
@@ -68,15 +53,6 @@ __global__ __launch_bounds__(kEngineThreads) void engine_fill_kernel(const int32
 }
 
 }  // namespace
-
-hipError_t launch_engine_apply(const int32_t *stage, int bs, int n_upd, int max_blocks, int32_t *seq_lens,
-                               int32_t *block_table, hipStream_t stream)
-{
-    const int n = bs > n_upd ? bs : n_upd;
-    hipLaunchKernelGGL(engine_apply_kernel, dim3((n + kEngineThreads - 1) / kEngineThreads), dim3(kEngineThreads),
-                       0, stream, stage, bs, n_upd, max_blocks, seq_lens, block_table);
-    return hipGetLastError();
-}
 
 hipError_t launch_engine_fill(const int32_t *pages, int n_pages, int hkv, int head_dim, bool fp8, uint32_t seed,
                               void *k_pages, void *v_pages, float *k_scales, float *v_scales, hipStream_t stream)

@@ -162,6 +162,16 @@ struct AppendParams {
     float *k_scales;            // E4M3 only: [num_pages][Hkv]
     float *v_scales;
     int32_t batch, num_kv_heads, max_blocks, num_pages;
+    // Decode-engine mode (null otherwise): the step's lengths and the page of
+    // every sequence's new token are read from a staging buffer laid out as
+    // [lengths: B][token pages: B][block-table updates: n_upd x (slot, block,
+    // page)], and the same launch also stores the lengths in set_seq_lens and
+    // applies the updates to set_block_table for the attention that follows
+    // (seq_lens and block_table are not read).
+    const int32_t *stage;
+    int32_t n_upd;
+    int32_t *set_seq_lens;
+    int32_t *set_block_table;
 };
 
 constexpr int kMaxPrefixBatch = 4096;      // the fused prefix kernel keeps three ints per sequence in LDS
@@ -198,10 +208,7 @@ hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);
-// Decode engine helpers (engine.hip): apply a step's lengths and block-table
-// updates from a device staging buffer; fill prompt pages with synthetic data.
-hipError_t launch_engine_apply(const int32_t *stage, int bs, int n_upd, int max_blocks, int32_t *seq_lens,
-                               int32_t *block_table, hipStream_t stream);
+// Decode engine helper (engine.hip): fill prompt pages with synthetic data.
 hipError_t launch_engine_fill(const int32_t *pages, int n_pages, int hkv, int head_dim, bool fp8, uint32_t seed,
                               void *k_pages, void *v_pages, float *k_scales, float *v_scales, hipStream_t stream);
 // Resident split-kernel workgroups per CU (occupancy query), for the default worker count.
