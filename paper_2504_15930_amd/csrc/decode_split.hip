@@ -8,14 +8,22 @@ namespace {
 
 // Every workgroup derives the tile stream from the lengths and the block
 // table (its dynamic LDS holds the page prefix sum and the lengths).
+//
+// Worker w = wave * gridDim.x + block: the four wavefronts of a workgroup take
+// ranges a quarter of the stream apart, so a CU streams four unrelated
+// sequences or heads at once rather than four neighbouring ranges of one
+// unit (whose tiles all sit at the same offset inside their pages), and a
+// stream too small for every worker still spreads over as many CUs as it
+// has workers.
 template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void split_kv_kernel(SplitParams p)
 {
     extern __shared__ int32_t s_dyn[];
-    int32_t *const s_cum = s_dyn;              // [B + 1]
+    int32_t *const s_cum = s_dyn;                // [B + 1]
     int32_t *const s_len = s_dyn + p.batch + 1;  // [B]
     scan_sequences(p, s_cum, s_len);
-    split_unit_worker<D, FP8, kAllPages>(p, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    split_unit_worker<D, FP8, kAllPages>(p, wave * (int)gridDim.x + (int)blockIdx.x,
                                          StreamLds{s_cum, s_len, nullptr, nullptr});
 }
 
