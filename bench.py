@@ -278,7 +278,8 @@ def traffic_bytes(workload: str) -> float | None:
 
 
 def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
-    """Time the oracle on a growing seeded sample of sequences until ~target_s of CPU work."""
+    """Time the oracle on a growing seeded sample of sequences until ~target_s of CPU work; when
+    the whole batch takes less than half of that, time repeated passes over it instead."""
     import torch
 
     import oracle
@@ -289,7 +290,7 @@ def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
     Hkv = batch.k_pages.shape[1]
     kvb = 1 if batch.kv_dtype == "e4m3" else 2
 
-    def run(rows):
+    def run(rows, passes=1):
         bt = batch.block_table[rows].cpu().numpy()
         lens = L[rows]
         nb = -(-np.maximum(lens, 0) // 16)
@@ -312,8 +313,9 @@ def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
             kw = dict(k_scales=batch.k_scales.index_select(0, idx).cpu().numpy(),
                       v_scales=batch.v_scales.index_select(0, idx).cpu().numpy())
         t0 = time.perf_counter()
-        ref = oracle.decode_attn(args["q"], args["k_pages"], args["v_pages"], new_bt, lens,
-                                 batch.scale, threads=threads, **kw)
+        for _ in range(passes):
+            ref = oracle.decode_attn(args["q"], args["k_pages"], args["v_pages"], new_bt, lens,
+                                     batch.scale, threads=threads, **kw)
         return ref, time.perf_counter() - t0
 
     n = 1
@@ -326,14 +328,18 @@ def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
         n = int(min(len(L), max(n + 1, np.searchsorted(cum, want_tokens) + 1)))
         rows = order[:n]
         ref, dt = run(rows)
-    nbytes = algorithmic_bytes(L[rows], Hq, Hkv, D, kvb)
+    passes = 1
+    if n == len(L) and dt < target_s / 2:   # the whole batch is quick: repeat it
+        passes = max(2, int(round(target_s / max(dt, 1e-3))))
+        ref, dt = run(rows, passes)
+    nbytes = algorithmic_bytes(L[rows], Hq, Hkv, D, kvb) * passes
     g = out_gpu[rows].float().cpu().double().numpy()
     err = float(np.abs(g - ref).max())
     rel = float((np.sqrt(((g - ref) ** 2).sum(-1)) / np.maximum(np.sqrt((ref ** 2).sum(-1)), 1e-30)).max())
     return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", cores=oracle.max_threads(threads),
                 kind="oracle", seconds=round(dt, 3),
                 sample=f"{len(rows)} of {len(L)} sequences ({int(L[rows].sum())} tokens, "
-                       f"{nbytes / 1e6:.1f} MB algorithmic), seeded choice",
+                       f"{nbytes / passes / 1e6:.1f} MB algorithmic), seeded choice, {passes} pass(es)",
                 parity_vs_gpu=dict(max_abs_err=err, max_row_rel_l2=rel))
 
 

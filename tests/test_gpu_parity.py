@@ -63,6 +63,35 @@ def test_random_shapes(shape, workers, kv):
     assert_parity(out, oracle_full(b), f"{shape} workers={workers} {kv}")
 
 
+def _sweep_case(i):
+    """Configuration i of the seeded sweep: head layout, head size, batch, a length mix with the
+    edge values (0, 1, 15, 16, 17, whole pages, long tails), worker count and cache type."""
+    rng = np.random.default_rng(1000 + i)
+    D = int(rng.choice([64, 128]))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 16]))
+    B = int(rng.choice([1, 2, 3, 8, 31, 64, 130, 257]))
+    kind = rng.integers(0, 4, B)   # 0: edge value, 1: short, 2: lognormal tail, 3: whole pages
+    L = np.where(kind == 0, rng.choice([0, 1, 15, 16, 17, 31, 32, 33], B),
+         np.where(kind == 1, rng.integers(1, 64, B),
+         np.where(kind == 2, np.minimum(np.exp(rng.normal(np.log(300), 1.2, B)).astype(np.int64) + 1, 6000),
+                  16 * rng.integers(1, 40, B))))
+    workers = int(rng.choice([0, 0, 1, 2, 5, 33, 256, 1000]))
+    kv = str(rng.choice(["bf16", "e4m3"]))
+    return L.astype(np.int64), G * Hkv, Hkv, D, workers, kv
+
+
+@pytest.mark.parametrize("i", range(40))
+def test_seeded_sweep(i):
+    L, Hq, Hkv, D, workers, kv = _sweep_case(i)
+    what = f"sweep {i}: B={len(L)} Hq={Hq} Hkv={Hkv} D={D} workers={workers} {kv} total={int(L.sum())}"
+    _say(what)
+    b = inputs.make_paged_batch(L, Hq, Hkv, D, seed=2000 + i, device=DEV, kv_dtype=kv)
+    out = sl.run_batch(b, num_workers=workers)
+    torch.cuda.synchronize()
+    assert_parity(out, oracle_full(b), what)
+
+
 @pytest.mark.parametrize("workers", [1, 3, 16, 97, 1000, 0])
 def test_sparse_batch_with_empty_runs(workers):
     """Mostly empty sequences, including the first and the last, with the non-empty ones far apart:

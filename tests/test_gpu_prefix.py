@@ -159,3 +159,34 @@ def test_max_prefix_batch_many_groups():
     ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
                              case["scale"])
     parity.assert_parity(out, ref, "batch 4096, 2048 groups")
+
+
+def _prefix_sweep_case(i):
+    """Configuration i of the seeded prefix sweep: head layout, group sizes (some too large to
+    share), prompt lengths (some under one page), generated lengths, extra unshared sequences and
+    worker count."""
+    rng = np.random.default_rng(3000 + i)
+    D = int(rng.choice([64, 128]))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 7, 8]))
+    ng = int(rng.integers(1, 9))
+    members = [int(rng.choice([1, 2, 3, 5, 8, 16, 20])) for _ in range(ng)]
+    prompts = [int(rng.choice([5, 16, 40, 100, 256, 700])) for _ in range(ng)]
+    gen = int(rng.choice([0, 20, 200]))
+    extra = int(rng.integers(0, 4))
+    workers = int(rng.choice([0, 0, 1, 7, 100, 1000]))
+    return members, prompts, gen, G * Hkv, Hkv, D, extra, workers
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_prefix_seeded_sweep(i):
+    members, prompts, gen, Hq, Hkv, D, extra, workers = _prefix_sweep_case(i)
+    what = f"prefix sweep {i}: members={members} prompts={prompts} gen<={gen} Hq={Hq} Hkv={Hkv} D={D} " \
+           f"extra={extra} workers={workers}"
+    print(what, flush=True)
+    rng = np.random.default_rng(4000 + i)
+    case, starts, shared = grpo_case(rng, members, prompts, gen, Hq, Hkv, D, extra)
+    out = run_prefix(case, starts, shared, workers)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, what)
