@@ -312,39 +312,50 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
         pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
     }
 
-    // Value rows as bf16 dwords: row r holds D/16 consecutive elements.
-    constexpr int RW = D / 32;   // bf16 dwords per row
-    uint32_t vb[4 * RW];
-    if constexpr (FP8) {
+    // Value operands. Lane (n, quad) holds D/16 consecutive elements of the
+    // value rows of tokens 4 quad + r (r = 0..3); value block i takes element i
+    // of the four rows, rows 0-1 in its low dword and rows 2-3 in the high one.
+    // Byte permutes gather them: bf16 halves directly, E4M3 codes in pairs of
+    // rows before one widening per two blocks. Dead slots (only in a
+    // sequence's last page) hold arbitrary cache contents and are zeroed first,
+    // as 0 * NaN would poison the MFMA.
+    constexpr int VR = Tile<D, FP8>::VW / 4;   // dwords per row
+    uint32_t vr[4 * VR];
+#pragma unroll
+    for (int k = 0; k < 4 * VR; ++k)
+        vr[k] = t.v[k];
+    if (valid < kPageSize) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
-            for (int c = 0; c < D / 64; ++c)
-                e4m3x4_to_bf16(t.v[r * (D / 64) + c], vb[r * RW + 2 * c], vb[r * RW + 2 * c + 1]);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4 * RW; ++i)
-            vb[i] = t.v[i];
-    }
-    uint32_t mlo = 0xffffffffu, mhi = 0xffffffffu;
-    if (valid < kPageSize) {   // zero dead rows: their slots may hold NaN
-        const int t0 = 4 * quad;
-        mlo = (t0 + 0 < valid ? 0x0000ffffu : 0u) | (t0 + 1 < valid ? 0xffff0000u : 0u);
-        mhi = (t0 + 2 < valid ? 0x0000ffffu : 0u) | (t0 + 3 < valid ? 0xffff0000u : 0u);
+            for (int c = 0; c < VR; ++c)
+                vr[r * VR + c] = 4 * quad + r < valid ? vr[r * VR + c] : 0u;
     }
 #pragma unroll
-    for (int i = 0; i < D / 16; ++i) {
-        const int w = i >> 1;
-        uint32_t lo, hi;
-        if ((i & 1) == 0) {
-            lo = (vb[0 * RW + w] & 0xffffu) | (vb[1 * RW + w] << 16);
-            hi = (vb[2 * RW + w] & 0xffffu) | (vb[3 * RW + w] << 16);
+    for (int i = 0; i < D / 16; i += 2) {
+        uint32_t lo0, lo1, hi0, hi1;
+        if constexpr (FP8) {
+            // Bytes (row a, row b) of elements i and i + 1, then one widening per element.
+            const int c = i / 4;
+            const uint32_t sel = (i % 4) == 0 ? 0x05010400u : 0x07030602u;
+            const uint32_t p01 = __builtin_amdgcn_perm(vr[VR + c], vr[c], sel);
+            const uint32_t p23 = __builtin_amdgcn_perm(vr[3 * VR + c], vr[2 * VR + c], sel);
+            lo0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(p01, 1.0f, false));
+            lo1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(p01, 1.0f, true));
+            hi0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(p23, 1.0f, false));
+            hi1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(p23, 1.0f, true));
         } else {
-            lo = (vb[0 * RW + w] >> 16) | (vb[1 * RW + w] & 0xffff0000u);
-            hi = (vb[2 * RW + w] >> 16) | (vb[3 * RW + w] & 0xffff0000u);
+            // Dword w holds elements 2w (low half) and 2w + 1 (high half) of a row.
+            const int w = i / 2;
+            lo0 = __builtin_amdgcn_perm(vr[VR + w], vr[w], 0x05040100u);
+            lo1 = __builtin_amdgcn_perm(vr[VR + w], vr[w], 0x07060302u);
+            hi0 = __builtin_amdgcn_perm(vr[3 * VR + w], vr[2 * VR + w], 0x05040100u);
+            hi1 = __builtin_amdgcn_perm(vr[3 * VR + w], vr[2 * VR + w], 0x07060302u);
         }
-        const i16x4_t va = __builtin_bit_cast(i16x4_t, u32x2_t{lo & mlo, hi & mhi});
-        st.acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb, st.acc[i], 0, 0, 0);
+        st.acc[i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, u32x2_t{lo0, hi0}), pb,
+                                                              st.acc[i], 0, 0, 0);
+        st.acc[i + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, u32x2_t{lo1, hi1}),
+                                                                  pb, st.acc[i + 1], 0, 0, 0);
     }
 }
 
