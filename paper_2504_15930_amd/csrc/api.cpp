@@ -343,8 +343,10 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.cum_out = nullptr;   // the sums go through pp
     sp_.max_blocks = d->max_blocks_per_seq;
     sp_.num_pages = d->num_pages;
-    // Shared-page pass: one workgroup of four wavefronts per worker.
+    // Shared-page pass: one workgroup of four wavefronts per worker; up to
+    // twice the base count when own-page workgroups are idle.
     const int nws = shared_workers(nw);
+    const int nws_max = nw > 2 * nws ? 2 * nws : (nw > nws ? nw : nws);   // slots are sized for nw workers
     SplitParams shp = sp_;
     shp.num_workers = nws;
     shp.part_ml = ws.shared_ml;
@@ -359,7 +361,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.unit_acc = ws.own_unit_acc;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
-    if (launch_prefix_split(sp_, shp, pp, d->head_dim, d->stream) != hipSuccess)
+    if (launch_prefix_split(sp_, shp, nws_max, pp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
         return SL_ERR_HIP;
@@ -387,6 +389,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     mp.group = G;
     mp.num_workers = nw;
     mp.num_shared_workers = nws;
+    mp.max_shared_workers = nws_max;
     mp.max_blocks = d->max_blocks_per_seq;
     if (launch_merge_prefix(mp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;

@@ -488,7 +488,8 @@ __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const P
 // LDS (3 B + 2 NG + 2 ints).
 template <int D>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(SplitParams own, SplitParams shared,
-                                                                               PrefixParams pp, int own_blocks)
+                                                                               PrefixParams pp, int own_blocks,
+                                                                               int max_shared)
 {
     extern __shared__ int32_t s_dyn[];
     const int B = own.batch, NG = pp.num_groups;
@@ -502,23 +503,29 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(Sp
         split_unit_worker<D, false, kOwnPages>(
             own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
             StreamLds{s_own, s_len, s_group, s_sh});
-    else
-        split_shared_worker<D>(shared, (int)blockIdx.x - own_blocks, SharedLds{s_sh, s_gl, NG});
+    else {
+        SplitParams sh = shared;
+        sh.num_workers = effective_shared_workers((long long)s_own[B] * own.num_kv_heads, own.num_workers,
+                                                  shared.num_workers, max_shared);
+        split_shared_worker<D>(sh, (int)blockIdx.x - own_blocks, SharedLds{s_sh, s_gl, NG});
+    }
 }
 
 }  // namespace
 
-hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, const PrefixParams &pp,
-                               int head_dim, hipStream_t stream)
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int max_shared,
+                               const PrefixParams &pp, int head_dim, hipStream_t stream)
 {
     const int own_blocks = (own.num_workers + kWavesPerBlock - 1) / kWavesPerBlock;
-    const dim3 grid(own_blocks + shared.num_workers);
+    const dim3 grid(own_blocks + max_shared);
     const dim3 block(kWave * kWavesPerBlock);
     const size_t lds = prefix_dynamic_lds(own.batch, pp.num_groups);
     if (head_dim == 128)
-        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, lds, stream, own, shared, pp, own_blocks);
+        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, lds, stream, own, shared, pp, own_blocks,
+                           max_shared);
     else if (head_dim == 64)
-        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, lds, stream, own, shared, pp, own_blocks);
+        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, lds, stream, own, shared, pp, own_blocks,
+                           max_shared);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -230,7 +230,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
     }
     if (sk == 0 && n_o == 1)
         return;   // finished by a single worker
-    const long long nw_s = tot_s > 0 ? effective_workers(tot_s, p.num_shared_workers) : 1;
+    const long long nw_s =
+        tot_s > 0 ? effective_workers(tot_s, effective_shared_workers(tot_o, p.num_workers, p.num_shared_workers,
+                                                                      p.max_shared_workers))
+                  : 1;
     long long a_s = 0;
     int wf_s = 0, n_s = 0, row = 0;
     if (sk > 0) {

@@ -57,6 +57,22 @@ __host__ __device__ inline int effective_workers(long long total, int num_worker
     const long long want = (total + kMinTilesPerWorker - 1) / kMinTilesPerWorker;
     return want < 1 ? 1 : (want < num_workers ? (int)want : num_workers);
 }
+// Prefix sharing: shared-page workgroups that take part in a call. The launch
+// holds the own-page workgroups and up to twice `base` shared ones, and a CU
+// holds two such workgroups; own-page workgroups without work exit at once,
+// and a shared workgroup beyond `base` takes such an idle slot, so a batch with
+// few own pages still streams its shared pages with two workgroups per CU.
+// The split kernel and the merge derive it from the same totals (own tiles).
+__host__ __device__ inline int effective_shared_workers(long long own_total, int own_workers, int base,
+                                                        int max_workers)
+{
+    const int own_blocks = (own_workers + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int active =
+        own_total > 0 ? (effective_workers(own_total, own_workers) + kWavesPerBlock - 1) / kWavesPerBlock : 0;
+    const int idle = own_blocks - active;
+    const int n = base + (idle < base ? idle : base);
+    return n < max_workers ? n : max_workers;
+}
 constexpr size_t kAlign = 256;
 
 // Tile metadata, one wave-uniform word per tile, from bit 0:
@@ -140,7 +156,8 @@ struct PrefixMergeParams {
     const float *shared_unit_ml, *shared_unit_acc;  // [B Hkv][kPrefixRows][2 | D]: whole shared units
     uint16_t *out;
     int32_t batch, num_groups, num_q_heads, num_kv_heads, group, num_workers, max_blocks;
-    int32_t num_shared_workers;   // workgroups of the shared-page pass
+    int32_t num_shared_workers;   // base and largest count of shared-page workgroups
+    int32_t max_shared_workers;   // (effective_shared_workers)
 };
 
 struct MergeParams {
@@ -201,10 +218,11 @@ inline size_t prefix_dynamic_lds(int batch, int num_groups)
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Prefix mode: the own-page pass (single-unit workers) and the shared-page
 // pass (one workgroup of kPrefixBlocks wavefronts per worker, one 16-row
-// column block each, partial states only; shared.num_workers counts
-// workgroups) in one launch, followed by the merge.
-hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, const PrefixParams &pp,
-                               int head_dim, hipStream_t stream);
+// column block each, partial states only) in one launch, followed by the
+// merge. shared.num_workers is the base count of shared workgroups and
+// max_shared the largest (effective_shared_workers).
+hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int max_shared,
+                               const PrefixParams &pp, int head_dim, hipStream_t stream);
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);
