@@ -149,14 +149,19 @@ __device__ __forceinline__ void compute(State<D> &st, const uint8_t *stage, cons
 #pragma unroll
     for (int r = 0; r < 4; ++r)
         sc[r] = s4[r] * score_mul;
-    const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-    if (mx > st.m + kRescaleSlack) {
-        const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a piece's first tile
-        st.l *= alpha;
+    // Cross-lane maximum only when a lane exceeds the running maximum by the
+    // slack (a wave-wide vote), as in the single-unit worker.
+    const float lmx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    if (__builtin_amdgcn_ballot_w64(lmx > st.m + kRescaleSlack) != 0) {
+        const float mx = quad_max(lmx);
+        if (mx > st.m + kRescaleSlack) {
+            const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a piece's first tile
+            st.l *= alpha;
 #pragma unroll
-        for (int i = 0; i < D / 16; ++i)
-            st.acc[i] *= alpha;
-        st.m = mx;
+            for (int i = 0; i < D / 16; ++i)
+                st.acc[i] *= alpha;
+            st.m = mx;
+        }
     }
     float pr[4];
 #pragma unroll

@@ -287,14 +287,20 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
             if (4 * quad + r >= valid)
                 sc[r] = kNegInf;
     }
-    const float mx = quad_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
-    if (mx > st.m + kRescaleSlack) {
-        const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a unit's first tile
-        st.l *= alpha;
+    // The head's maximum over the tile (four lanes) is needed only when one of
+    // them exceeds the running maximum by the slack: a wave-wide vote skips
+    // the cross-lane exchange on the other tiles, with the same result.
+    const float lmx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    if (__builtin_amdgcn_ballot_w64(lmx > st.m + kRescaleSlack) != 0) {
+        const float mx = quad_max(lmx);
+        if (mx > st.m + kRescaleSlack) {
+            const float alpha = __builtin_amdgcn_exp2f(st.m - mx);   // 0 on a unit's first tile
+            st.l *= alpha;
 #pragma unroll
-        for (int i = 0; i < D / 16; ++i)
-            st.acc[i] *= alpha;
-        st.m = mx;
+            for (int i = 0; i < D / 16; ++i)
+                st.acc[i] *= alpha;
+            st.m = mx;
+        }
     }
     float pr[4];
 #pragma unroll
