@@ -6,7 +6,9 @@
 // tiles (see sl_internal.h) as a flat sequence, keeping an online-softmax
 // state for the G query heads of the unit (sequence, KV head) the current tile
 // belongs to, and finishing that unit whenever its last tile, or the end of
-// the range, is reached.
+// the range, is reached. For the shared pages of prefix-shared attention the
+// four wavefronts of a workgroup stream the same range, each computing one
+// 16-row column block of the shared unit's query rows (kSharedPages).
 //
 // Per 16-token tile, with lane = n + 16 * quad (n = lane & 15, quad = lane >> 4):
 //
@@ -29,10 +31,10 @@
 // ~6.0 TB/s instead of ~6.85 TB/s on MI355X, so K is read in whole 1 KB runs
 // and regrouped through a small per-wave LDS buffer. Both are streamed with
 // non-temporal loads. Tiles are software-pipelined kNbuf deep;
-// the tile-list entry (page and unit metadata) of a tile is fetched one
-// pipeline turn before the tile itself, and the query rows of a unit are
-// loaded together with the unit's first tile, so the stream never waits on a
-// dependent load, also across unit boundaries.
+// the block-table entry of a tile (its unit metadata comes from a cursor over
+// the units) is fetched one pipeline turn before the tile itself, and the
+// query rows of a unit are loaded together with the unit's first tile, so the
+// stream never waits on a dependent load, also across unit boundaries.
 //
 // FP8 pages hold OCP E4M3 codes; they are widened to bf16 exactly
 // (v_cvt_scalef32_pk_bf16_fp8 with unit scale), the per-(page, head) key
@@ -133,11 +135,20 @@ __device__ __forceinline__ int q_index(int s, int quad)
     return FP8 ? quad * (D / 4) + 8 * s : 32 * s + 8 * quad;
 }
 
-// Issue every load of one tile. All loads are unconditional.
-template <int D, bool FP8>
+// Issue every load of one tile. All loads are unconditional. K/V are streamed
+// with non-temporal loads (STREAM) unless the tile is read by several
+// wavefronts at once (the column blocks of a shared unit), where plain loads
+// let the siblings find it in L2. `blk` < 0: a single-unit tile, whose query
+// rows are the group's G heads; `blk` >= 0: column block blk of a shared unit
+// (rows 16 blk + n, member r / G and head r % G of the group).
+template <int D, bool FP8, bool STREAM = true>
 __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p, int32_t page,
-                                           uint32_t meta, bool with_q, int n, int quad, int lane)
+                                           uint32_t meta, bool with_q, int n, int quad, int lane, int blk = -1)
 {
+    auto ld128_kv = [](const uint8_t *a) { return STREAM ? ld128_stream(a) : ld128(a); };
+    auto ld64_kv = [](const uint8_t *a) {
+        return STREAM ? ld64_stream(a) : *reinterpret_cast<const u32x2_t *>(a);
+    };
     constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
     t.meta = meta;
     t.bad_page = page < 0;
@@ -149,7 +160,7 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     // regrouped into the score-MFMA layout through LDS when the tile is used.
 #pragma unroll
     for (int i = 0; i < Tile<D, FP8>::KW / 4; ++i) {
-        const u32x4_t x = ld128_stream(kt + 1024 * i + 16 * lane);
+        const u32x4_t x = ld128_kv(kt + 1024 * i + 16 * lane);
 #pragma unroll
         for (int c = 0; c < 4; ++c)
             t.k[4 * i + c] = x[c];
@@ -159,12 +170,12 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
         for (int r = 0; r < 4; ++r) {
             const uint8_t *src = vt + ((4 * quad + r) * D + n * (D / 16)) * 2;
             if constexpr (D == 128) {
-                const u32x4_t x = ld128_stream(src);
+                const u32x4_t x = ld128_kv(src);
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
                     t.v[4 * r + c] = x[c];
             } else {
-                const u32x2_t x = ld64_stream(src);
+                const u32x2_t x = ld64_kv(src);
                 t.v[2 * r] = x[0];
                 t.v[2 * r + 1] = x[1];
             }
@@ -189,7 +200,12 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     // when the operand is formed.
     if (with_q) {
         const int G = p.group;
-        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)min(n, G - 1)) * D;
+        int rel = min(n, G - 1);
+        if (blk >= 0) {   // rows past the shared unit's read its first row (never written out)
+            const int r = 16 * blk + n;
+            rel = r < ((int)(meta & 15u) + 1) * G ? (r / G) * p.num_q_heads + r % G : 0;
+        }
+        const uint16_t *qrow = p.q + ((size_t)(meta >> kMetaRowShift) + (size_t)rel) * D;
 #pragma unroll
         for (int s = 0; s < D / 32; ++s)
             t.q[s] = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
@@ -365,6 +381,24 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
     }
 }
 
+// Store this lane's share of a partial state (m, l, acc) as row `row` of
+// (part_ml [][2], part_acc [][D]); l is the head's full sum (quad_sum).
+template <int D>
+__device__ __forceinline__ void store_partial(const Piece<D> &st, float l, bool bad, float *part_ml,
+                                              float *part_acc, size_t row, int quad)
+{
+    const float poison = bad ? __builtin_nanf("") : 0.0f;
+    float *dst = part_acc + row * D + quad * (D / 4);
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < D / 16; i += 4)
+            *reinterpret_cast<f32x4_t *>(dst + r * (D / 16) + i) =
+                f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
+    if (quad == 0)   // a NaN maximum keeps the poison alive through the merge weights
+        *reinterpret_cast<f32x2_t *>(part_ml + row * 2) = f32x2_t{st.m + poison, l};
+}
+
 // Finish the current unit: normalise and write its bf16 rows if the whole unit
 // was seen and nothing else is merged into it (`full`), else store the partial
 // state, G rows, in slot `slot` of (part_ml, part_acc).
@@ -396,17 +430,7 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
             *reinterpret_cast<u32x4_t *>(dst + 16 * c) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
         }
     } else {
-        const float poison = bad ? __builtin_nanf("") : 0.0f;
-        float *dst = part_acc + (slot * G + n) * D + d0;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int i = 0; i < D / 16; i += 4)
-                *reinterpret_cast<f32x4_t *>(dst + r * (D / 16) + i) =
-                    f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
-        if (quad == 0)   // a NaN maximum keeps the poison alive through the merge weights
-            *reinterpret_cast<f32x2_t *>(part_ml + (slot * G + n) * 2) =
-                f32x2_t{st.m + poison, l};
+        store_partial<D>(st, l, bad, part_ml, part_acc, slot * G + n, quad);
     }
 }
 
@@ -478,29 +502,39 @@ __device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_
             p.cum_out[b] = s_cum[b];
 }
 
-// Which tiles a single-unit worker streams.
-constexpr int kAllPages = 0;   // plain attention: every page of every sequence
-constexpr int kOwnPages = 1;   // prefix sharing: the pages after each sequence's shared ones
+// Which tiles a worker streams.
+constexpr int kAllPages = 0;      // plain attention: every page of every sequence
+constexpr int kOwnPages = 1;      // prefix sharing: the pages after each sequence's shared ones
+constexpr int kSharedPages = 2;   // prefix sharing: each group's shared pages once, one column block per wavefront
 
 // LDS view of the unit stream: the exclusive prefix sum of tiles per sequence
 // and the lengths; for kOwnPages also each sequence's group and the groups'
 // shared-page prefix sum (a sequence's own pages start after its group's
-// shared pages).
+// shared pages). For kSharedPages `cum` is the shared-page prefix sum over the
+// groups and `gl` each group's first member and size, packed as
+// lead | (members - 1) << 16.
 struct StreamLds {
-    const int32_t *cum;     // [B + 1]
+    const int32_t *cum;     // [B + 1], or [NG + 1] for kSharedPages
     const int32_t *len;     // [B]
     const int32_t *group;   // [B], kOwnPages only (-1: no shared pages)
     const int32_t *sh;      // [NG + 1], kOwnPages only
+    const int32_t *gl;      // [NG], kSharedPages only
+    int32_t num_groups;     // kSharedPages only
 };
 
-// Worker w (one wavefront) of the single-unit split-KV pass over the stream
-// that `sv` describes (in LDS, complete: the caller has passed a barrier).
+// Worker w of the split-KV pass over the stream that `sv` describes (in LDS,
+// complete: the caller has passed a barrier). A worker is one wavefront, or
+// for kSharedPages the four wavefronts of a workgroup, which stream the same
+// tiles and compute column blocks blk = 0..3 of each shared unit.
 template <int D, bool FP8, int MODE>
-__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, const StreamLds &sv)
+__device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, const StreamLds &sv, int blk = -1)
 {
+    static_assert(MODE != kSharedPages || !FP8, "prefix sharing reads a bf16 cache");
+    constexpr bool kShared = MODE == kSharedPages;
     if (w >= p.num_workers)
         return;
-    const long long total = (long long)sv.cum[p.batch] * p.num_kv_heads;
+    const int nseq = kShared ? sv.num_groups : p.batch;   // "sequences" of the stream
+    const long long total = (long long)sv.cum[nseq] * p.num_kv_heads;
     const int nw = effective_workers(total, p.num_workers);
     if (w >= nw)
         return;
@@ -535,7 +569,7 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
         }
     };
     // Largest b with Hkv cum[b] <= s0 (then its n_b > 0).
-    int blo = 0, bhi = p.batch;
+    int blo = 0, bhi = nseq;
     while (bhi - blo > 1) {
         const int mid = (blo + bhi) >> 1;
         if ((long long)sv.cum[mid] * p.num_kv_heads <= s0)
@@ -545,26 +579,36 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     }
     int cb = blo;
     int cnb = sv.cum[cb + 1] - sv.cum[cb];
-    int clen = sv.len[cb];
+    int clen = kShared ? sv.gl[cb] : sv.len[cb];   // kSharedPages: the group's packed lead and size
     int csh = shared_of(cb);
     const int off = (int)(s0 - (long long)sv.cum[cb] * p.num_kv_heads);
     int cg = off / cnb;
     int cj = off - cg * cnb;
     const int max_len = p.max_blocks * kPageSize;
     auto entry = [&](int i) -> u32x4_t {
-        const int pg = csh + cj;   // page index in the sequence
-        const uint32_t bt = __builtin_bit_cast(
-            uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (cb * p.max_blocks + pg) * 4, 0));
-        const int live = min(kPageSize, clen - pg * kPageSize);
-        uint32_t meta = (uint32_t)(max(live, 1) - 1) | ((uint32_t)(cb * p.num_q_heads + cg * G) << kMetaRowShift);
+        uint32_t bt, meta;
+        if constexpr (kShared) {
+            // Page cj of the group's shared pages, read through its first member's row; the
+            // count field holds members - 1 (every shared page is full).
+            const int lead = clen & 0xffff;
+            bt = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (lead * p.max_blocks + cj) * 4, 0));
+            meta = (uint32_t)(clen >> 16) | ((uint32_t)(lead * p.num_q_heads + cg * G) << kMetaRowShift);
+        } else {
+            const int pg = csh + cj;   // page index in the sequence
+            bt = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_raw_buffer_load_b32(btab, 0, (cb * p.max_blocks + pg) * 4, 0));
+            const int live = min(kPageSize, clen - pg * kPageSize);
+            meta = (uint32_t)(max(live, 1) - 1) | ((uint32_t)(cb * p.num_q_heads + cg * G) << kMetaRowShift);
+            if (clen > max_len)
+                meta |= kMetaBadLen;
+            if (csh > 0)
+                meta |= kMetaPrefixed;
+        }
         if (cj == 0)
             meta |= kMetaFirst;
         if (cj == cnb - 1)
             meta |= kMetaLast;
-        if (clen > max_len)
-            meta |= kMetaBadLen;
-        if (csh > 0)
-            meta |= kMetaPrefixed;
         const u32x4_t e = {bt, meta, (uint32_t)cg, 0u};
         if (i < ntiles - 1) {   // advance to the next tile of the stream
             if (++cj == cnb) {
@@ -575,7 +619,7 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
                         ++cb;
                     while (sv.cum[cb + 1] == sv.cum[cb]);   // tiles remain, so a sequence with tiles follows
                     cnb = sv.cum[cb + 1] - sv.cum[cb];
-                    clen = sv.len[cb];
+                    clen = kShared ? sv.gl[cb] : sv.len[cb];
                     csh = shared_of(cb);
                 }
             }
@@ -615,8 +659,8 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     Tile<D, FP8> buf[kNbuf];
 #pragma unroll
     for (int k = 0; k < kNbuf - 1; ++k)
-        issue_tile<D, FP8>(buf[k], p, first_page[k], first_meta[k],
-                           k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane);
+        issue_tile<D, FP8, !kShared>(buf[k], p, first_page[k], first_meta[k],
+                                     k == 0 || (first_meta[k] & kMetaFirst) != 0, n, quad, lane, blk);
 
     Piece<D> st;
     reset(st);
@@ -629,8 +673,8 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
         for (int k = 0; k < kNbuf; ++k) {
             const int i = i0 + k;
             const uint32_t next_meta = meta_of(ring[k]);
-            issue_tile<D, FP8>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
-                               (next_meta & kMetaFirst) != 0, n, quad, lane);
+            issue_tile<D, FP8, !kShared>(buf[(k + kNbuf - 1) % kNbuf], p, page_of(ring[k]), next_meta,
+                                         (next_meta & kMetaFirst) != 0, n, quad, lane, blk);
             ring[k] = entry(i + 2 * kNbuf - 1);
             if (i < ntiles) {
                 const Tile<D, FP8> &t = buf[k];
@@ -638,12 +682,30 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
                 if (i == 0 || (meta & kMetaFirst) != 0) {
 #pragma unroll
                     for (int s = 0; s < D / 32; ++s)
-                        qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
+                        qop[s] = __builtin_bit_cast(bf16x8_t,
+                                                    kShared || n < G ? t.q[s] : u32x4_t{0u, 0u, 0u, 0u});
                 }
                 started |= (meta & kMetaFirst) != 0;
                 bad |= t.bad_page || (meta & kMetaBadLen) != 0;
-                compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(meta & 15u) + 1, lds, lane, n, quad);
-                if ((meta & kMetaLast) != 0 || i == ntiles - 1) {
+                compute_tile<D, FP8>(st, t, qop, p.scale_log2, kShared ? kPageSize : (int)(meta & 15u) + 1, lds,
+                                     lane, n, quad);
+                if (kShared && ((meta & kMetaLast) != 0 || i == ntiles - 1)) {
+                    // A shared unit's state is always merged: a whole one goes to the unit area
+                    // (indexed by first query row / G), a cut one to the worker's slot; block blk
+                    // holds rows 16 blk .. 16 blk + 15 of the unit's kPrefixRows.
+                    const uint32_t row0 = meta >> kMetaRowShift;
+                    const bool whole = started && (meta & kMetaLast) != 0;
+                    const size_t slot = whole ? (size_t)(row0 / (uint32_t)G) : 2 * (size_t)w + slot_sel;
+                    const int r = 16 * blk + n;
+                    const float l = quad_sum(st.l);
+                    if (r < ((int)(meta & 15u) + 1) * G)
+                        store_partial<D>(st, l, bad, whole ? p.unit_ml : p.part_ml, whole ? p.unit_acc : p.part_acc,
+                                         slot * kPrefixRows + r, quad);
+                    reset(st);
+                    started = false;
+                    bad = false;
+                    slot_sel = 1;
+                } else if (!kShared && ((meta & kMetaLast) != 0 || i == ntiles - 1)) {
                     // A unit cut by this range leaves its piece in the worker's slot 2w + slot_sel.
                     // A whole unit is written out, unless it still has to be merged (shared pages,
                     // or the own pages of a sequence that has them): then its state goes to its
