@@ -22,13 +22,17 @@
  * page; a finished sample's pages return to the stack last block first.
  *
  * Every step, on desc.stream and in this order: new prompt pages are filled;
- * one KV-append launch stores the step's new K/V rows (the caller's k_new /
- * v_new buffers, the same every step, with the quantise-on-write of
- * sl_kv_append_fp8 for an E4M3 cache) and also writes the step's sequence
- * lengths and new block-table entries into seq_lens and block_table, all read
- * by the device from a mapped pinned staging buffer; sl_decode_attn (or _fp8)
- * computes the step's attention output into `out` with the caller's q. Slots
- * without a sample have length 0 (zero output rows).
+ * the step's new K/V rows are stored (the caller's k_new / v_new buffers, the
+ * same every step, with the quantise-on-write of sl_kv_append_fp8 for an
+ * E4M3 cache) and the step's sequence lengths and new block-table entries are
+ * written into seq_lens and block_table, all read by the device from a mapped
+ * pinned staging buffer; the step's attention output (sl_decode_attn or
+ * _fp8) is computed into `out` with the caller's q. Slots without a sample
+ * have length 0 (zero output rows). Within one sl_engine_run call the next
+ * step's rows and bookkeeping are written by the launch that finishes this
+ * step's attention (after it has read the cache), unless that step admits
+ * prompts; when the call returns, the buffers hold the state after its last
+ * step.
  *
  * The schedule is fixed by the lengths given at creation, so the host never
  * waits for the device during a run: steps are enqueued asynchronously, and

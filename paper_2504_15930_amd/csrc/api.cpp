@@ -5,6 +5,7 @@
 #include <mutex>
 
 #include "../../include/sl.h"
+#include "api_internal.h"
 #include "sl_internal.h"
 
 namespace sl {
@@ -156,7 +157,7 @@ bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 
 sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, const void *v_pages,
               const float *k_scales, const float *v_scales, const int32_t *block_table,
-              const int32_t *seq_lens, float scale, uint16_t *out, bool fp8)
+              const int32_t *seq_lens, float scale, uint16_t *out, bool fp8, const AppendParams *next = nullptr)
 {
     sl_status st = check_desc(d);
     if (st != SL_OK)
@@ -226,6 +227,11 @@ sl_status run(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, con
     mp.num_kv_heads = d->num_kv_heads;
     mp.group = G;
     mp.num_workers = nw;
+    mp.next_kind = 0;
+    if (next) {
+        mp.next = *next;
+        mp.next_kind = fp8 ? 2 : 1;
+    }
     if (launch_merge(mp, d->head_dim, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     return SL_OK;
@@ -397,6 +403,15 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
 }
 
 }  // namespace
+
+sl_status decode_attn_then_append(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, const void *v_pages,
+                                  const float *k_scales, const float *v_scales, const int32_t *block_table,
+                                  const int32_t *seq_lens, float scale, uint16_t *out, bool fp8,
+                                  const AppendParams *next)
+{
+    return run(d, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, out, fp8, next);
+}
+
 }  // namespace sl
 
 extern "C" {

@@ -4,13 +4,18 @@
 // into BS slots, pages come from a LIFO free stack, and the lengths given at
 // creation fix every step in advance. Each step is packed into a pinned
 // staging buffer ([seq_lens][page of each new token][block-table updates]
-// [prompt pages to fill]), followed by the launches on the caller's stream:
-// fill (only when a prompt was admitted), KV append (which also applies the
-// step's lengths and block-table updates) and decode attention. The fill and
-// append kernels read the staging buffer in place (mapped pinned memory),
-// which saves a copy command per step; a ring of such buffers, each reused
-// only once the kernels that read it have completed, lets the host run ahead
-// of the GPU.
+// [prompt pages to fill]). On the caller's stream a step is: its
+// bookkeeping and KV append (the lengths and block-table updates applied,
+// the new K/V rows stored), then decode attention (split kernel and merge).
+// Since the host knows the next step before the GPU has run this one, the
+// next step's bookkeeping and append run in this step's merge launch, after
+// the attention has read the cache: a step costs two launches. A step that
+// admits prompts fills their pages first (fill kernel) and runs its own
+// append launch, and so does the first step of each sl_engine_run call. The
+// kernels read the staging buffer in place (mapped pinned memory), which
+// saves a copy command per step; a ring of such buffers, each reused only
+// once the kernels that read it have completed, lets the host run ahead of
+// the GPU.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -18,6 +23,7 @@
 
 #include "sl.h"
 #include "sl_engine.h"
+#include "api_internal.h"
 #include "sl_internal.h"
 
 namespace {
@@ -63,10 +69,22 @@ struct sl_engine {
         }
     }
 
-    sl_status one_step();
+    // A step's staging: ring slot, update and fill counts, active samples.
+    struct Staged {
+        int ring = 0, n_upd = 0, n_fill = 0, n_active = 0;
+    };
+    // The next step's staging: not prepared yet, prepared but not launched
+    // (it admits prompts), or applied and appended by the last merge launch.
+    enum { kNone, kPrepared, kLaunched } next_state = kNone;
+    Staged next;
+
+    sl_status prepare(Staged &out);
+    sl::AppendParams append_params(const Staged &sg) const;
+    sl_status launch_staged(const Staged &sg);
+    sl_status one_step(bool chain);
 };
 
-sl_status sl_engine::one_step()
+sl_status sl_engine::prepare(Staged &out)
 {
     // Refill free slots, lowest first, taking prompt pages in block order.
     std::vector<int32_t> upd;    // (slot, block, page) triples
@@ -89,19 +107,19 @@ sl_status sl_engine::one_step()
             fills.push_back(pg);
         }
     }
-    int n_active = 0;
+    out.n_active = 0;
     for (int b = 0; b < BS; ++b)
-        n_active += occupant[b] >= 0;
-    if (n_active == 0) {
-        done = true;
+        out.n_active += occupant[b] >= 0;
+    if (out.n_active == 0)
         return SL_OK;
-    }
 
-    // This step's lengths, and a new page for every token that opens one.
+    // This step's lengths, the page of every slot's new token, and a new page
+    // for every token that opens one.
     const int r = ring;
     ring = (ring + 1) % kRing;
     if (ev_pending[r] && hipEventSynchronize(ev[r]) != hipSuccess)
         return SL_ERR_HIP;
+    ev_pending[r] = false;
     int32_t *h = h_stage[r];
     for (int b = 0; b < BS; ++b) {
         const int i = occupant[b];
@@ -120,17 +138,16 @@ sl_status sl_engine::one_step()
         h[b] = t + 1;
         h[BS + b] = pages[b][t / kPageSize];
     }
-    const int n_upd = (int)upd.size() / 3;
-    const int n_fill = (int)fills.size();
+    out.ring = r;
+    out.n_upd = (int)upd.size() / 3;
+    out.n_fill = (int)fills.size();
     std::memcpy(h + 2 * BS, upd.data(), sizeof(int32_t) * upd.size());
     std::memcpy(h + 2 * BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
-    hipStream_t s = step_desc.stream;
-    const int32_t *ds = d_stage[r];
-    // Prompt data first: the new token of an admitted sample may land in its last prompt page.
-    if (n_fill > 0 &&
-        sl::launch_engine_fill(ds + 2 * BS + 3 * n_upd, n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
-                               buf.k_scales, buf.v_scales, s) != hipSuccess)
-        return SL_ERR_HIP;
+    return SL_OK;
+}
+
+sl::AppendParams sl_engine::append_params(const Staged &sg) const
+{
     sl::AppendParams ap;
     ap.k_new = buf.k_new;
     ap.v_new = buf.v_new;
@@ -144,30 +161,55 @@ sl_status sl_engine::one_step()
     ap.num_kv_heads = Hkv;
     ap.max_blocks = max_blocks;
     ap.num_pages = num_pages;
-    ap.stage = ds;
-    ap.n_upd = n_upd;
+    ap.stage = d_stage[sg.ring];
+    ap.n_upd = sg.n_upd;
     ap.set_seq_lens = buf.seq_lens;
     ap.set_block_table = buf.block_table;
-    if (sl::launch_append(ap, D, fp8, s) != hipSuccess)
-        return SL_ERR_HIP;
-    if (hipEventRecord(ev[r], s) != hipSuccess)   // the staging buffer is free again after this
-        return SL_ERR_HIP;
-    ev_pending[r] = true;
-    sl_status st;
-    if (fp8)
-        st = sl_decode_attn_fp8(&step_desc, buf.q, static_cast<const uint8_t *>(buf.k_pages),
-                                static_cast<const uint8_t *>(buf.v_pages), buf.k_scales, buf.v_scales,
-                                buf.block_table, buf.seq_lens, attn_scale, buf.out);
-    else
-        st = sl_decode_attn(&step_desc, buf.q, static_cast<const uint16_t *>(buf.k_pages),
-                            static_cast<const uint16_t *>(buf.v_pages), buf.block_table, buf.seq_lens,
-                            attn_scale, buf.out);
-    if (st != SL_OK)
-        return st;
+    return ap;
+}
 
-    // The step ran: every occupied slot made one token; finished samples
-    // leave and give their pages back, last block first.
-    active.push_back(n_active);
+sl_status sl_engine::launch_staged(const Staged &sg)
+{
+    hipStream_t s = step_desc.stream;
+    const int32_t *ds = d_stage[sg.ring];
+    // Prompt data first: the new token of an admitted sample may land in its last prompt page.
+    if (sg.n_fill > 0 &&
+        sl::launch_engine_fill(ds + 2 * BS + 3 * sg.n_upd, sg.n_fill, Hkv, D, fp8, seed, buf.k_pages, buf.v_pages,
+                               buf.k_scales, buf.v_scales, s) != hipSuccess)
+        return SL_ERR_HIP;
+    if (sl::launch_append(append_params(sg), D, fp8, s) != hipSuccess)
+        return SL_ERR_HIP;
+    if (hipEventRecord(ev[sg.ring], s) != hipSuccess)   // the staging buffer is free again after this
+        return SL_ERR_HIP;
+    ev_pending[sg.ring] = true;
+    return SL_OK;
+}
+
+sl_status sl_engine::one_step(bool chain)
+{
+    // This step's bookkeeping and KV append: launched now, unless the previous
+    // step's merge already ran them.
+    sl_status st;
+    Staged cur = next;
+    if (next_state == kNone) {
+        st = prepare(cur);
+        if (st != SL_OK)
+            return st;
+        if (cur.n_active == 0) {
+            done = true;
+            return SL_OK;
+        }
+    }
+    if (next_state != kLaunched) {
+        st = launch_staged(cur);
+        if (st != SL_OK)
+            return st;
+    }
+    next_state = kNone;
+
+    // The step's tokens are decided: every occupied slot makes one; finished
+    // samples leave and give their pages back, last block first.
+    active.push_back(cur.n_active);
     for (int b = 0; b < BS; ++b) {
         const int i = occupant[b];
         if (i < 0)
@@ -181,6 +223,43 @@ sl_status sl_engine::one_step()
         }
     }
     ++step;
+
+    // With more steps to run, stage the next one now. Its bookkeeping and KV
+    // append then run in this step's merge launch, after the attention has
+    // read the cache, unless it admits prompts: their pages must be filled
+    // before the append, so that step launches them itself.
+    const sl::AppendParams *fused = nullptr;
+    sl::AppendParams nap;
+    bool last = false;
+    if (chain) {
+        st = prepare(next);
+        if (st != SL_OK)
+            return st;
+        if (next.n_active == 0) {
+            last = true;
+        } else if (next.n_fill == 0) {
+            nap = append_params(next);
+            fused = &nap;
+            next_state = kLaunched;
+        } else {
+            next_state = kPrepared;
+        }
+    }
+    if (fp8)
+        st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, buf.k_scales, buf.v_scales,
+                                         buf.block_table, buf.seq_lens, attn_scale, buf.out, true, fused);
+    else
+        st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, nullptr, nullptr,
+                                         buf.block_table, buf.seq_lens, attn_scale, buf.out, false, fused);
+    if (st != SL_OK)
+        return st;
+    if (fused) {
+        if (hipEventRecord(ev[next.ring], step_desc.stream) != hipSuccess)
+            return SL_ERR_HIP;
+        ev_pending[next.ring] = true;
+    }
+    if (last)
+        done = true;
     return SL_OK;
 }
 
@@ -286,7 +365,7 @@ sl_status sl_engine_run(sl_engine *e, int32_t max_steps, int32_t *steps_run)
         return e->failed;
     for (int k = 0; k < max_steps && !e->done; ++k) {
         const int before = e->step;
-        const sl_status st = e->one_step();
+        const sl_status st = e->one_step(k + 1 < max_steps);
         if (st != SL_OK) {
             e->failed = st;
             return st;

@@ -15,7 +15,7 @@
 // loads. Units finished by a single worker were already written and are
 // skipped. Sequences without pages get zero rows (NaN rows for an invalid
 // negative length), which no split-KV worker visits.
-#include "sl_internal.h"
+#include "append_unit.h"
 
 namespace sl {
 namespace {
@@ -51,11 +51,23 @@ __device__ __forceinline__ long long div_floor(long long x, long long y)
     return q;
 }
 
-template <int D>
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p)
+// NEXT: the decode engine's next-step append in the same launch (0 none,
+// 1 bf16 cache, 2 E4M3 cache), in the workgroups after the merge's.
+template <int D, int NEXT>
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p, int merge_blocks)
 {
     constexpr int E = D / kWave;   // output columns per lane (1 or 2)
     constexpr int kBatch = 8;      // pieces whose rows are fetched together with the weights
+    if constexpr (NEXT != 0) {
+        if ((int)blockIdx.x >= merge_blocks) {
+            const int ab = (int)blockIdx.x - merge_blocks;
+            apply_stage(p.next, ab * kMergeThreads + threadIdx.x, ((int)gridDim.x - merge_blocks) * kMergeThreads);
+            const int unit = ab * (kMergeThreads / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+            if (unit < p.next.batch * p.next.num_kv_heads)
+                append_unit<D, NEXT == 2>(p.next, unit, threadIdx.x & (kWave - 1));
+            return;
+        }
+    }
     const int Hkv = p.num_kv_heads;
     const int G = p.group;
     const int item = blockIdx.x * (kMergeThreads / kWave) +
@@ -364,13 +376,27 @@ hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream)
 {
     const long long items = (long long)p.batch * p.num_kv_heads * p.group;
     const int per_block = kMergeThreads / kWave;
-    const dim3 grid((unsigned)((items + per_block - 1) / per_block));
-    if (head_dim == 128)
-        hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(kMergeThreads), 0, stream, p);
-    else if (head_dim == 64)
-        hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(kMergeThreads), 0, stream, p);
+    const int merge_blocks = (int)((items + per_block - 1) / per_block);
+    const int next_blocks =
+        p.next_kind != 0 ? (int)(((long long)p.next.batch * p.next.num_kv_heads + per_block - 1) / per_block) : 0;
+    const dim3 grid((unsigned)(merge_blocks + next_blocks));
+    const dim3 block(kMergeThreads);
+#define SL_MERGE(DD, NN) hipLaunchKernelGGL((merge_kernel<DD, NN>), grid, block, 0, stream, p, merge_blocks)
+    if (head_dim == 128 && p.next_kind == 0)
+        SL_MERGE(128, 0);
+    else if (head_dim == 128 && p.next_kind == 1)
+        SL_MERGE(128, 1);
+    else if (head_dim == 128 && p.next_kind == 2)
+        SL_MERGE(128, 2);
+    else if (head_dim == 64 && p.next_kind == 0)
+        SL_MERGE(64, 0);
+    else if (head_dim == 64 && p.next_kind == 1)
+        SL_MERGE(64, 1);
+    else if (head_dim == 64 && p.next_kind == 2)
+        SL_MERGE(64, 2);
     else
         return hipErrorInvalidValue;
+#undef SL_MERGE
     return hipGetLastError();
 }
 

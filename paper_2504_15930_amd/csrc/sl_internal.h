@@ -160,15 +160,6 @@ struct PrefixMergeParams {
     int32_t max_shared_workers;   // (effective_shared_workers)
 };
 
-struct MergeParams {
-    const int32_t *seq_lens;
-    const int32_t *cum_pages;
-    const float *part_ml;
-    const float *part_acc;
-    uint16_t *out;
-    int32_t batch, num_q_heads, num_kv_heads, group, num_workers;
-};
-
 struct AppendParams {
     const uint16_t *k_new;      // [B][Hkv][D] bf16 rows of the step's new token
     const uint16_t *v_new;
@@ -190,6 +181,23 @@ struct AppendParams {
     int32_t *set_seq_lens;
     int32_t *set_block_table;
 };
+
+struct MergeParams {
+    const int32_t *seq_lens;
+    const int32_t *cum_pages;
+    const float *part_ml;
+    const float *part_acc;
+    uint16_t *out;
+    int32_t batch, num_q_heads, num_kv_heads, group, num_workers;
+    // Decode engine: the next step's staged append (and its bookkeeping) runs
+    // in the same launch, in workgroups after the merge's; 0 none, 1 bf16
+    // cache, 2 E4M3 cache. The merge never reads what it writes: it reads the
+    // lengths only for sequences without pages, whose rows are zero whatever
+    // the step (the engine's lengths are never negative).
+    AppendParams next;
+    int32_t next_kind;
+};
+
 
 constexpr int kMaxPrefixBatch = 4096;      // the fused prefix kernel keeps three ints per sequence in LDS
 
