@@ -131,12 +131,12 @@ sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
     DeviceInfo *info = nullptr;
     if (device_info(&info) != hipSuccess)
         return SL_ERR_HIP;
-    // One split-KV workgroup (four workers, one per SIMD) per CU streams the
-    // bf16 cache at the best measured rate on MI355X; two waves per SIMD were
-    // slower, and any count that is not a multiple of the CU count leaves some
-    // CUs with more workers than others. FP8 tiles carry half the bytes for
-    // the same conversion and MFMA work, so two workgroups per CU hide it better.
-    const int want = fp8 ? 2 : 1;
+    // One split-KV workgroup (four workers, one per SIMD) per CU streams
+    // both caches at the best measured rate on MI355X; two waves per SIMD were
+    // slower (bf16 by 4%, E4M3 by 1-4%), and any count that is not a multiple
+    // of the CU count leaves some CUs with more workers than others.
+    const int want = 1;
+    (void)fp8;
     const int blocks = info->blocks[d->head_dim == 128][fp8 ? 1 : 0];
     *nw = info->cus * (blocks < want ? (blocks > 0 ? blocks : 1) : want) * kWavesPerBlock;
     if (*nw > kMaxWorkers)

@@ -30,7 +30,7 @@
 // line per instruction (each row spread over four lanes), which streams at
 // ~6.0 TB/s instead of ~6.85 TB/s on MI355X, so K is read in whole 1 KB runs
 // and regrouped through a small per-wave LDS buffer. Both are streamed with
-// non-temporal loads. Tiles are software-pipelined kNbuf deep;
+// non-temporal loads. Tiles are software-pipelined (pipeline_depth);
 // the block-table entry of a tile (its unit metadata comes from a cursor over
 // the units) is fetched one pipeline turn before the tile itself, and the
 // query rows of a unit are loaded together with the unit's first tile, so the
@@ -59,10 +59,11 @@ constexpr float kNegInf = -__builtin_inff();
 // more than this slack (base-2 units), which bounds the weights by 2^8 and
 // leaves the accumulators untouched on most tiles after a unit's first.
 constexpr float kRescaleSlack = 8.0f;
-#ifndef SL_NBUF
-#define SL_NBUF 2
-#endif
-constexpr int kNbuf = SL_NBUF;               // tiles in the software pipeline
+// Tiles in the software pipeline: two for a bf16 cache (three and four
+// measured the same); three for E4M3, whose tiles carry half the bytes for
+// the same work per tile.
+template <bool FP8>
+constexpr int pipeline_depth() { return FP8 ? 3 : 2; }
 constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit buffer resource (CDNA3/4)
 
 __device__ __forceinline__ u32x4_t ld128(const uint8_t *p) { return *reinterpret_cast<const u32x4_t *>(p); }
@@ -531,6 +532,7 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
 {
     static_assert(MODE != kSharedPages || !FP8, "prefix sharing reads a bf16 cache");
     constexpr bool kShared = MODE == kSharedPages;
+    constexpr int kNbuf = pipeline_depth<FP8>();
     if (w >= p.num_workers)
         return;
     const int nseq = kShared ? sv.num_groups : p.batch;   // "sequences" of the stream
