@@ -84,10 +84,10 @@ typedef struct sl_attn_desc {
     int32_t max_blocks_per_seq; /* row length of block_table */
     int32_t num_pages;          /* pages in each pool; valid page ids are [0, num_pages) */
     int32_t num_workers;        /* split-KV workers (wavefronts). 0: library default
-                                   (four per CU for bf16, eight for FP8, bounded by
-                                   occupancy); 1..65536: exactly this many. The result
-                                   does not depend on it beyond fp32 rounding; tests
-                                   vary it to exercise the merge. */
+                                   (three per CU for bf16, four per CU for FP8 and for
+                                   prefix-shared attention); 1..65536: exactly this
+                                   many. The result does not depend on it beyond fp32
+                                   rounding; tests vary it to exercise the merge. */
     hipStream_t stream;         /* stream the work is enqueued on (0: null stream) */
     void *workspace;            /* device scratch, >= sl_decode_attn_workspace_size bytes,
                                    256-byte aligned; contents need no initialisation */

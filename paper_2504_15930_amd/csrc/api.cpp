@@ -122,7 +122,7 @@ sl_status check_desc(const sl_attn_desc *d)
     return SL_OK;
 }
 
-sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
+sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw, bool prefix = false)
 {
     if (d->num_workers > 0) {
         *nw = d->num_workers;
@@ -131,14 +131,17 @@ sl_status resolve_workers(const sl_attn_desc *d, bool fp8, int *nw)
     DeviceInfo *info = nullptr;
     if (device_info(&info) != hipSuccess)
         return SL_ERR_HIP;
-    // One split-KV workgroup (four workers, one per SIMD) per CU streams
-    // both caches at the best measured rate on MI355X; two waves per SIMD were
-    // slower (bf16 by 4%, E4M3 by 1-4%), and any count that is not a multiple
-    // of the CU count leaves some CUs with more workers than others.
-    const int want = 1;
-    (void)fp8;
+    // Split-KV workgroups of four workers (one per SIMD), measured on
+    // MI355X: the E4M3 cache streams best with one per CU; the bf16 cache,
+    // whose tiles carry twice the bytes, already saturates HBM with three
+    // workgroups per four CUs (1.5-2.5% faster than one per CU, as fewer
+    // streams compete for the memory; 640 or fewer workers, or 1280 and more,
+    // were slower). Two waves per SIMD were slower for both. Prefix-shared
+    // attention keeps one own-page workgroup per CU beside its shared-page
+    // workgroups (three per four CUs was 12% slower).
     const int blocks = info->blocks[d->head_dim == 128][fp8 ? 1 : 0];
-    *nw = info->cus * (blocks < want ? (blocks > 0 ? blocks : 1) : want) * kWavesPerBlock;
+    const int per_cu4 = fp8 || prefix ? 4 : 3;   // workgroups per four CUs
+    *nw = (blocks > 0 ? info->cus * per_cu4 / 4 : info->cus) * kWavesPerBlock;
     if (*nw > kMaxWorkers)
         *nw = kMaxWorkers;
     return SL_OK;
@@ -308,7 +311,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
         !aligned4(seq_lens) || (num_groups > 0 && (!aligned4(group_start) || !aligned4(shared_pages))))
         return SL_ERR_ALIGNMENT;
     int nw = 0;
-    st = resolve_workers(d, false, &nw);
+    st = resolve_workers(d, false, &nw, true);
     if (st != SL_OK)
         return st;
     const int G = d->num_q_heads / d->num_kv_heads;
@@ -512,7 +515,7 @@ sl_status sl_decode_attn_prefix_workspace_size(const sl_attn_desc *desc, int32_t
     if (!bytes)
         return SL_ERR_NULL;
     int nw = 0;
-    st = sl::resolve_workers(desc, false, &nw);
+    st = sl::resolve_workers(desc, false, &nw, true);
     if (st != SL_OK)
         return st;
     *bytes = sl::prefix_workspace_layout(nullptr, desc->batch, desc->max_blocks_per_seq, desc->num_kv_heads,
