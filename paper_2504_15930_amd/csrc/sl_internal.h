@@ -1,7 +1,7 @@
 // Internal interface between the host-side entry points (api.cpp) and the
-// gfx950 kernels (decode_split.hip with the worker in decode_unit.h,
-// decode_shared.hip, merge.hip, append.hip, engine.hip), and
-// the decode engine (engine.cpp).
+// gfx950 kernels (decode_split.hip and decode_shared.hip with the worker in
+// decode_unit.h; append.hip and merge.hip with the append worker in
+// append_unit.h; engine.hip), and the decode engine (engine.cpp).
 //
 // Work decomposition. A "unit" is one (sequence b, KV head g) pair and owns
 // n_b = ceil(L_b / 16) page-head tiles (16 tokens x head_dim of one KV head).
@@ -20,6 +20,9 @@
 // partitioning launch and no tile list in memory. The block-table entry of a
 // tile is fetched a pipeline turn ahead, so unit boundaries inside the range
 // cost no dependent load and do not drain the load pipeline.
+//
+// (For the shared pages of prefix-shared attention a worker is a workgroup
+// whose four wavefronts stream the same range, one query block each.)
 //
 // A unit that lies inside one worker's range is finished by that worker; a
 // unit cut by a range boundary leaves one partial softmax state per worker
