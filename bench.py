@@ -183,11 +183,11 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
 
 
 def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
-    """Prefix sharing on a GRPO-like batch with this workload's heads: 32 prompts x 8 samples,
-    1024-token prompts (64 shared pages per group), generated lengths lognormal (median 512,
-    sigma 1, capped at 4096). Plain decode attention reads every sample's copy of the prompt
-    pages; the prefix path reads each group's once. ``unique_bytes`` counts what the prefix path
-    has to read (shared pages once per group)."""
+    """Prefix sharing on a GRPO-like batch with this workload's heads and cache type: 32 prompts
+    x 8 samples, 1024-token prompts (64 shared pages per group), generated lengths lognormal
+    (median 512, sigma 1, capped at 4096). Plain decode attention reads every sample's copy of the
+    prompt pages; the prefix path reads each group's once. ``unique_bytes`` counts what the prefix
+    path has to read (shared pages and their scales once per group)."""
     import torch
 
     from paper_2504_15930_amd import inputs, sl
@@ -195,24 +195,30 @@ def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
     prompts, samples, prompt_len = 32, 8, 1024
     b, starts, shared = inputs.make_grpo_batch(prompts, samples, prompt_len, seed=seed + 11, device=dev,
                                                num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
-                                               head_dim=w.head_dim)
+                                               head_dim=w.head_dim, kv_dtype=w.kv_dtype)
     torch.cuda.synchronize()
     L = b.seq_lens.cpu().numpy().astype(np.int64)
     Hq, Hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
-    plain_bytes = algorithmic_bytes(L, Hq, Hkv, D, 2)
+    kvb = 1 if w.kv_dtype == "e4m3" else 2
+    plain_bytes = algorithmic_bytes(L, Hq, Hkv, D, kvb)
     sp = prompt_len // 16
     own_tokens = int((L - 16 * sp).sum())
     own_pages = int((-(-L // 16) - sp).sum())
-    unique_bytes = ((prompts * sp * 16 + own_tokens) * Hkv * 2 * D * 2 + len(L) * 2 * Hq * D * 2
-                    + (prompts * sp + own_pages) * 4)
+    pages = prompts * sp + own_pages
+    unique_bytes = ((prompts * sp * 16 + own_tokens) * Hkv * 2 * D * kvb + len(L) * 2 * Hq * D * 2
+                    + pages * 4 + (pages * Hkv * 2 * 4 if kvb == 1 else 0))
     out = torch.empty_like(b.q)
 
     def plain():
         sl.run_batch(b, out=out)
 
     def prefixed():
-        sl.decode_attn_prefix(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, starts, shared,
-                              out=out)
+        if kvb == 1:
+            sl.decode_attn_prefix_fp8(b.q, b.k_pages, b.v_pages, b.k_scales, b.v_scales, b.block_table,
+                                      b.seq_lens, b.scale, starts, shared, out=out)
+        else:
+            sl.decode_attn_prefix(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, starts,
+                                  shared, out=out)
 
     res = {}
     for name, fn in (("plain", plain), ("prefix", prefixed)):
@@ -229,7 +235,8 @@ def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
         res[name] = e0.elapsed_time(e1) / steps
     return {
         "what": "decode attention with prefix sharing vs plain, GRPO-like batch",
-        "config": {"prompts": prompts, "samples": samples, "prompt_len": prompt_len, "gen_median": 512,
+        "config": {"kv_dtype": w.kv_dtype, "prompts": prompts, "samples": samples, "prompt_len": prompt_len,
+                   "gen_median": 512,
                    "gen_sigma": 1.0, "gen_cap": 4096, "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D,
                    "total_tokens": int(L.sum()), "max_seq_len": int(L.max())},
         "plain_ms": round(res["plain"], 5),
@@ -529,7 +536,7 @@ def main(argv=None) -> int:
         "GBps": round((nbytes + app_bytes) / (decode_ms * 1e-3) / 1e9, 2),
     }
 
-    if args.prefix and kvb == 2:
+    if args.prefix:
         print("[bench] prefix sharing", file=sys.stderr, flush=True)
         result["prefix"] = prefix_experiment(w, args.seed, dev, args.steps, args.warmup)
     if args.generation:

@@ -175,7 +175,23 @@ sl_status sl_decode_attn_prefix(const sl_attn_desc *desc, const uint16_t *q,
                                 const int32_t *group_start, const int32_t *shared_pages,
                                 int32_t num_groups, float scale, uint16_t *out);
 
-/* Workspace bytes sl_decode_attn_prefix needs for desc and num_groups. */
+/*
+ * Prefix sharing over an FP8 E4M3 cache: the pages, codes and per-(page, KV
+ * head) scales of sl_decode_attn_fp8, the groups of sl_decode_attn_prefix,
+ * and the same result as sl_decode_attn_fp8 on the same arguments (a shared
+ * page's scales are read once, from its own entry). k_scales and v_scales
+ * are device float [num_pages][Hkv], 4-byte aligned. Everything else, the
+ * workspace and the errors are as sl_decode_attn_prefix.
+ */
+sl_status sl_decode_attn_prefix_fp8(const sl_attn_desc *desc, const uint16_t *q,
+                                    const uint8_t *k_pages, const uint8_t *v_pages,
+                                    const float *k_scales, const float *v_scales,
+                                    const int32_t *block_table, const int32_t *seq_lens,
+                                    const int32_t *group_start, const int32_t *shared_pages,
+                                    int32_t num_groups, float scale, uint16_t *out);
+
+/* Workspace bytes sl_decode_attn_prefix and sl_decode_attn_prefix_fp8 need
+ * for desc and num_groups (one size serves both). */
 sl_status sl_decode_attn_prefix_workspace_size(const sl_attn_desc *desc, int32_t num_groups,
                                                size_t *bytes);
 

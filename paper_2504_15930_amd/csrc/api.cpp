@@ -295,9 +295,10 @@ sl_status check_prefix(const sl_attn_desc *d, int32_t num_groups)
     return SL_OK;
 }
 
-sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k_pages, const uint16_t *v_pages,
-                     const int32_t *block_table, const int32_t *seq_lens, const int32_t *group_start,
-                     const int32_t *shared_pages, int32_t num_groups, float scale, uint16_t *out)
+sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const void *k_pages, const void *v_pages,
+                     const float *k_scales, const float *v_scales, const int32_t *block_table,
+                     const int32_t *seq_lens, const int32_t *group_start, const int32_t *shared_pages,
+                     int32_t num_groups, float scale, uint16_t *out, bool fp8)
 {
     sl_status st = check_prefix(d, num_groups);
     if (st != SL_OK)
@@ -305,13 +306,14 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     if (d->batch == 0)
         return SL_OK;
     if (!q || !k_pages || !v_pages || !block_table || !seq_lens || !out ||
-        (num_groups > 0 && (!group_start || !shared_pages)))
+        (num_groups > 0 && (!group_start || !shared_pages)) || (fp8 && (!k_scales || !v_scales)))
         return SL_ERR_NULL;
     if (!aligned16(q) || !aligned16(out) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned4(block_table) ||
-        !aligned4(seq_lens) || (num_groups > 0 && (!aligned4(group_start) || !aligned4(shared_pages))))
+        !aligned4(seq_lens) || (num_groups > 0 && (!aligned4(group_start) || !aligned4(shared_pages))) ||
+        (fp8 && (!aligned4(k_scales) || !aligned4(v_scales))))
         return SL_ERR_ALIGNMENT;
     int nw = 0;
-    st = resolve_workers(d, false, &nw, true);
+    st = resolve_workers(d, fp8, &nw, true);
     if (st != SL_OK)
         return st;
     const int G = d->num_q_heads / d->num_kv_heads;
@@ -338,8 +340,8 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.q = q;
     sp_.k_pages = k_pages;
     sp_.v_pages = v_pages;
-    sp_.k_scales = nullptr;
-    sp_.v_scales = nullptr;
+    sp_.k_scales = fp8 ? k_scales : nullptr;
+    sp_.v_scales = fp8 ? v_scales : nullptr;
     sp_.out = out;
     sp_.batch = d->batch;
     sp_.num_kv_heads = d->num_kv_heads;
@@ -370,7 +372,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const uint16_t *k
     sp_.unit_acc = ws.own_unit_acc;
     if (d->timing_start && hipEventRecord(d->timing_start, d->stream) != hipSuccess)
         return SL_ERR_HIP;
-    if (launch_prefix_split(sp_, shp, nws_max, pp, d->head_dim, d->stream) != hipSuccess)
+    if (launch_prefix_split(sp_, shp, nws_max, pp, d->head_dim, fp8, d->stream) != hipSuccess)
         return SL_ERR_HIP;
     if (d->timing_stop && hipEventRecord(d->timing_stop, d->stream) != hipSuccess)
         return SL_ERR_HIP;
@@ -514,10 +516,16 @@ sl_status sl_decode_attn_prefix_workspace_size(const sl_attn_desc *desc, int32_t
         return st;
     if (!bytes)
         return SL_ERR_NULL;
-    int nw = 0;
+    // Sized for the larger of the bf16 and E4M3 worker counts, so one
+    // workspace serves both entry points.
+    int nw = 0, nw_fp8 = 0;
     st = sl::resolve_workers(desc, false, &nw, true);
+    if (st == SL_OK)
+        st = sl::resolve_workers(desc, true, &nw_fp8, true);
     if (st != SL_OK)
         return st;
+    if (nw_fp8 > nw)
+        nw = nw_fp8;
     *bytes = sl::prefix_workspace_layout(nullptr, desc->batch, desc->max_blocks_per_seq, desc->num_kv_heads,
                                          desc->num_q_heads / desc->num_kv_heads, desc->head_dim, nw, num_groups,
                                          nullptr);
@@ -529,8 +537,17 @@ sl_status sl_decode_attn_prefix(const sl_attn_desc *desc, const uint16_t *q, con
                                 const int32_t *group_start, const int32_t *shared_pages, int32_t num_groups,
                                 float scale, uint16_t *out)
 {
-    return sl::run_prefix(desc, q, k_pages, v_pages, block_table, seq_lens, group_start, shared_pages, num_groups,
-                          scale, out);
+    return sl::run_prefix(desc, q, k_pages, v_pages, nullptr, nullptr, block_table, seq_lens, group_start,
+                          shared_pages, num_groups, scale, out, false);
+}
+
+sl_status sl_decode_attn_prefix_fp8(const sl_attn_desc *desc, const uint16_t *q, const uint8_t *k_pages,
+                                    const uint8_t *v_pages, const float *k_scales, const float *v_scales,
+                                    const int32_t *block_table, const int32_t *seq_lens, const int32_t *group_start,
+                                    const int32_t *shared_pages, int32_t num_groups, float scale, uint16_t *out)
+{
+    return sl::run_prefix(desc, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, group_start,
+                          shared_pages, num_groups, scale, out, true);
 }
 
 }  // extern "C"

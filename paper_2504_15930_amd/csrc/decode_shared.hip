@@ -90,7 +90,7 @@ __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const P
 // file). Every workgroup first derives both streams in its dynamic LDS
 // (3 B + 2 NG + 2 ints); the number of shared-page workers that take part is
 // effective_shared_workers of the own-page total, as in the merge.
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(SplitParams own, SplitParams shared,
                                                                                PrefixParams pp, int own_blocks,
                                                                                int max_shared)
@@ -104,14 +104,14 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(Sp
     int32_t *const s_gl = s_sh + NG + 1;     // [NG]
     scan_prefix_groups(own, pp, s_own, s_len, s_group, s_sh, s_gl);
     if ((int)blockIdx.x < own_blocks)
-        split_unit_worker<D, false, kOwnPages>(
+        split_unit_worker<D, FP8, kOwnPages>(
             own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
             StreamLds{s_own, s_len, s_group, s_sh});
     else {
         SplitParams sh = shared;
         sh.num_workers = effective_shared_workers((long long)s_own[B] * own.num_kv_heads, own.num_workers,
                                                   shared.num_workers, max_shared);
-        split_unit_worker<D, false, kSharedPages>(sh, (int)blockIdx.x - own_blocks,
+        split_unit_worker<D, FP8, kSharedPages>(sh, (int)blockIdx.x - own_blocks,
                                                   StreamLds{s_sh, nullptr, nullptr, nullptr, s_gl, NG},
                                                   __builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
     }
@@ -120,20 +120,25 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(Sp
 }  // namespace
 
 hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int max_shared,
-                               const PrefixParams &pp, int head_dim, hipStream_t stream)
+                               const PrefixParams &pp, int head_dim, bool fp8, hipStream_t stream)
 {
     const int own_blocks = (own.num_workers + kWavesPerBlock - 1) / kWavesPerBlock;
     const dim3 grid(own_blocks + max_shared);
     const dim3 block(kWave * kWavesPerBlock);
     const size_t lds = prefix_dynamic_lds(own.batch, pp.num_groups);
-    if (head_dim == 128)
-        hipLaunchKernelGGL(prefix_split_kernel<128>, grid, block, lds, stream, own, shared, pp, own_blocks,
-                           max_shared);
-    else if (head_dim == 64)
-        hipLaunchKernelGGL(prefix_split_kernel<64>, grid, block, lds, stream, own, shared, pp, own_blocks,
-                           max_shared);
+#define SL_PREFIX(DD, FF) \
+    hipLaunchKernelGGL((prefix_split_kernel<DD, FF>), grid, block, lds, stream, own, shared, pp, own_blocks, max_shared)
+    if (head_dim == 128 && !fp8)
+        SL_PREFIX(128, false);
+    else if (head_dim == 64 && !fp8)
+        SL_PREFIX(64, false);
+    else if (head_dim == 128 && fp8)
+        SL_PREFIX(128, true);
+    else if (head_dim == 64 && fp8)
+        SL_PREFIX(64, true);
     else
         return hipErrorInvalidValue;
+#undef SL_PREFIX
     return hipGetLastError();
 }
 

@@ -150,6 +150,9 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
     auto ld64_kv = [](const uint8_t *a) {
         return STREAM ? ld64_stream(a) : *reinterpret_cast<const u32x2_t *>(a);
     };
+    auto ld32_kv = [](const uint8_t *a) {
+        return STREAM ? ld32_stream(a) : *reinterpret_cast<const uint32_t *>(a);
+    };
     constexpr size_t kTileBytes = (size_t)kPageSize * D * (FP8 ? 1 : 2);
     t.meta = meta;
     t.bad_page = page < 0;
@@ -186,11 +189,11 @@ __device__ __forceinline__ void issue_tile(Tile<D, FP8> &t, const SplitParams &p
         for (int r = 0; r < 4; ++r) {
             const uint8_t *src = vt + (4 * quad + r) * D + n * (D / 16);
             if constexpr (D == 128) {
-                const u32x2_t x = ld64_stream(src);
+                const u32x2_t x = ld64_kv(src);
                 t.v[2 * r] = x[0];
                 t.v[2 * r + 1] = x[1];
             } else {
-                t.v[r] = ld32_stream(src);
+                t.v[r] = ld32_kv(src);
             }
         }
         const float *sp = (lane & 32) ? p.v_scales : p.k_scales;
@@ -530,7 +533,6 @@ struct StreamLds {
 template <int D, bool FP8, int MODE>
 __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, const StreamLds &sv, int blk = -1)
 {
-    static_assert(MODE != kSharedPages || !FP8, "prefix sharing reads a bf16 cache");
     constexpr bool kShared = MODE == kSharedPages;
     constexpr int kNbuf = pipeline_depth<FP8>();
     if (w >= p.num_workers)

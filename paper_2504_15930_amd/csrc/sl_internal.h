@@ -233,7 +233,7 @@ hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_
 // merge. shared.num_workers is the base count of shared workgroups and
 // max_shared the largest (effective_shared_workers).
 hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared, int max_shared,
-                               const PrefixParams &pp, int head_dim, hipStream_t stream);
+                               const PrefixParams &pp, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_merge_prefix(const PrefixMergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_merge(const MergeParams &p, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendParams &p, int head_dim, bool fp8, hipStream_t stream);

@@ -240,11 +240,12 @@ def quantize_e4m3(x: torch.Tensor, live: torch.Tensor, chunk: int = 1 << 13):
 def make_grpo_batch(num_prompts: int, samples: int, prompt_len: int, *, seed: int = 0, device="cpu",
                     num_q_heads: int = 28, num_kv_heads: int = 4, head_dim: int = 128,
                     gen_median: float = 512.0, gen_sigma: float = 1.0, gen_cap: int = 4096,
-                    poison: bool = True):
+                    poison: bool = True, kv_dtype: str = "bf16"):
     """A GRPO-like decode batch: ``samples`` consecutive sequences per prompt share the prompt's
     floor(prompt_len / 16) full pages (same page ids, hence the same tokens) and continue on
     pages of their own; each has generated floor(X) tokens, ln X ~ N(ln gen_median, gen_sigma^2),
-    clipped to [0, gen_cap]. Returns (batch, group_start [num_prompts + 1], shared_pages
+    clipped to [0, gen_cap]. ``kv_dtype`` "e4m3" stores the pages as E4M3 codes with
+    per-(page, KV head) scales. Returns (batch, group_start [num_prompts + 1], shared_pages
     [num_prompts]) with the two int32 tensors on ``device``."""
     rng = np.random.default_rng(seed)
     B = num_prompts * samples
@@ -266,7 +267,7 @@ def make_grpo_batch(num_prompts: int, samples: int, prompt_len: int, *, seed: in
             table[b, sp:sp + own[b]] = perm[pos:pos + own[b]]
             pos += own[b]
     batch = make_paged_batch(lengths, num_q_heads, num_kv_heads, head_dim, seed=seed, device=device,
-                             block_table=table, num_pages=total + 1, rng=rng, poison=poison,
+                             kv_dtype=kv_dtype, block_table=table, num_pages=total + 1, rng=rng, poison=poison,
                              meta=dict(workload="grpo", prompts=num_prompts, samples=samples, prompt_len=prompt_len))
     batch.poison_page = poison_page
     dev = torch.device(device)

@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_U
                 -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
            "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_decode_attn_prefix",
-           "sl_decode_attn_prefix_workspace_size", "sl_status_string"]
+           "sl_decode_attn_prefix_fp8", "sl_decode_attn_prefix_workspace_size", "sl_status_string"]
 # include/sl_engine.h (typed in engine.py)
 ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
 # include/sl_dispatch.h (typed in dispatch.py)
@@ -74,6 +74,7 @@ def load(path: str = LIBRARY) -> ctypes.CDLL:
     lib.sl_decode_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_float, P]
     lib.sl_kv_append.argtypes = [D, P, P, P, P, P, P]
     lib.sl_decode_attn_prefix.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_float, P]
+    lib.sl_decode_attn_prefix_fp8.argtypes = [D, P, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_float, P]
     lib.sl_decode_attn_prefix_workspace_size.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
     lib.sl_kv_append_fp8.argtypes = [D, P, P, P, P, P, P, P, P]
     lib.sl_status_string.argtypes = [ctypes.c_int]
@@ -272,20 +273,19 @@ def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages, *, k_scales
             _check(st, "sl_kv_append")
 
 
-def decode_attn_prefix(q, k_pages, v_pages, block_table, seq_lens, scale, group_start, shared_pages, *,
-                       out=None, num_workers=0, workspace=None, timing=None) -> torch.Tensor:
-    """``sl_decode_attn_prefix``: decode attention reading each group's shared pages once.
-
-    ``group_start`` (int32 [G+1]) and ``shared_pages`` (int32 [G]) are device tensors;
-    consecutive sequences of a group share their first ``shared_pages[k]`` pages.
-    """
+def _run_prefix(fp8, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, group_start,
+                shared_pages, out, num_workers, workspace, timing):
+    kv_dtype = torch.uint8 if fp8 else torch.bfloat16
     _need(q, "q", torch.bfloat16, 3)
-    _need(k_pages, "k_pages", torch.bfloat16, 4)
-    _need(v_pages, "v_pages", torch.bfloat16, 4)
+    _need(k_pages, "k_pages", kv_dtype, 4)
+    _need(v_pages, "v_pages", kv_dtype, 4)
     _need(block_table, "block_table", torch.int32, 2)
     _need(seq_lens, "seq_lens", torch.int32, 1)
     _need(group_start, "group_start", torch.int32, 1)
     _need(shared_pages, "shared_pages", torch.int32, 1)
+    if fp8:
+        _need(k_scales, "k_scales", torch.float32, 2)
+        _need(v_scales, "v_scales", torch.float32, 2)
     ng = shared_pages.shape[0]
     if group_start.shape[0] != ng + 1:
         raise ValueError("group_start must have num_groups + 1 entries")
@@ -293,8 +293,14 @@ def decode_attn_prefix(q, k_pages, v_pages, block_table, seq_lens, scale, group_
     N, Hkv, P, D2 = k_pages.shape
     if D2 != D or v_pages.shape != k_pages.shape or block_table.shape[0] != B or seq_lens.shape[0] != B:
         raise ValueError("shape mismatch")
+    if fp8 and (tuple(k_scales.shape) != (N, Hkv) or tuple(v_scales.shape) != (N, Hkv)):
+        raise ValueError("scales must have shape [num_pages, num_kv_heads]")
     if out is None:
         out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 3)
+        if out.shape != q.shape:
+            raise ValueError("out must have the shape of q")
     lib = load()
     with torch.cuda.device(q.device):
         stream = torch.cuda.current_stream(q.device).cuda_stream
@@ -309,8 +315,35 @@ def decode_attn_prefix(q, k_pages, v_pages, block_table, seq_lens, scale, group_
         desc.workspace_bytes = ws.numel() * ws.element_size()
         if timing is not None:
             desc.timing_start, desc.timing_stop = timing
-        _check(lib.sl_decode_attn_prefix(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
-                                         block_table.data_ptr(), seq_lens.data_ptr(), group_start.data_ptr(),
-                                         shared_pages.data_ptr(), ng, float(scale), out.data_ptr()),
-               "sl_decode_attn_prefix")
+        if fp8:
+            _check(lib.sl_decode_attn_prefix_fp8(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(),
+                                                 v_pages.data_ptr(), k_scales.data_ptr(), v_scales.data_ptr(),
+                                                 block_table.data_ptr(), seq_lens.data_ptr(),
+                                                 group_start.data_ptr(), shared_pages.data_ptr(), ng,
+                                                 float(scale), out.data_ptr()),
+                   "sl_decode_attn_prefix_fp8")
+        else:
+            _check(lib.sl_decode_attn_prefix(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(),
+                                             v_pages.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
+                                             group_start.data_ptr(), shared_pages.data_ptr(), ng, float(scale),
+                                             out.data_ptr()),
+                   "sl_decode_attn_prefix")
     return out
+
+
+def decode_attn_prefix(q, k_pages, v_pages, block_table, seq_lens, scale, group_start, shared_pages, *,
+                       out=None, num_workers=0, workspace=None, timing=None) -> torch.Tensor:
+    """``sl_decode_attn_prefix``: decode attention reading each group's shared pages once.
+
+    ``group_start`` (int32 [G+1]) and ``shared_pages`` (int32 [G]) are device tensors;
+    consecutive sequences of a group share their first ``shared_pages[k]`` pages.
+    """
+    return _run_prefix(False, q, k_pages, v_pages, None, None, block_table, seq_lens, scale, group_start,
+                       shared_pages, out, num_workers, workspace, timing)
+
+
+def decode_attn_prefix_fp8(q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, group_start,
+                           shared_pages, *, out=None, num_workers=0, workspace=None, timing=None) -> torch.Tensor:
+    """``sl_decode_attn_prefix_fp8``: prefix sharing over uint8 E4M3 pages with fp32 [N, Hkv] scales."""
+    return _run_prefix(True, q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, group_start,
+                       shared_pages, out, num_workers, workspace, timing)

@@ -18,10 +18,11 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
 
-def grpo_case(rng, members, prompts, gen_max, Hq, Hkv, D, extra=0, shared_override=None):
+def grpo_layout(rng, members, prompts, gen_max, extra=0):
     """Groups of `members[k]` sequences whose first floor(prompts[k] / 16) pages are the same
     page ids (and tokens); each member continues with `gen` tokens on pages of its own; `extra`
-    unshared sequences follow."""
+    unshared sequences follow. Returns (lengths, block table, pool size, group_start,
+    shared_pages)."""
     lengths, starts, shared = [], [0], []
     for m, p in zip(members, prompts):
         lengths += [p + int(g) for g in rng.integers(0, gen_max + 1, m)]
@@ -43,10 +44,29 @@ def grpo_case(rng, members, prompts, gen_max, Hq, Hkv, D, extra=0, shared_overri
     for b in range(starts[-1], B):
         for i in range(mb):
             table[b, i] = perm.pop()
-    if shared_override is not None:
-        shared = shared_override
-    case, dense = pins.random_case(rng, B, Hq, Hkv, D, 16, lengths, table=table)
-    return case, np.array(starts, np.int32), np.array(shared, np.int32)
+    return lengths, table, N, np.array(starts, np.int32), np.array(shared, np.int32)
+
+
+def grpo_case(rng, members, prompts, gen_max, Hq, Hkv, D, extra=0):
+    """A bf16 oracle case over grpo_layout's groups."""
+    lengths, table, N, starts, shared = grpo_layout(rng, members, prompts, gen_max, extra)
+    case, dense = pins.random_case(rng, len(lengths), Hq, Hkv, D, 16, lengths, table=table)
+    return case, starts, shared
+
+
+def grpo_fp8_batch(rng, members, prompts, gen_max, Hq, Hkv, D, extra=0, seed=0):
+    """An E4M3 device batch over grpo_layout's groups (codes and per-(page, KV head) scales)."""
+    lengths, table, N, starts, shared = grpo_layout(rng, members, prompts, gen_max, extra)
+    b = inputs.make_paged_batch(np.array(lengths), Hq, Hkv, D, seed=seed, device=DEV, kv_dtype="e4m3",
+                                block_table=table, num_pages=N)
+    return b, torch.from_numpy(starts).to(DEV), torch.from_numpy(shared).to(DEV)
+
+
+def run_prefix_fp8(b, starts, shared, num_workers=0):
+    out = sl.decode_attn_prefix_fp8(b.q, b.k_pages, b.v_pages, b.k_scales, b.v_scales, b.block_table, b.seq_lens,
+                                    b.scale, starts, shared, num_workers=num_workers)
+    torch.cuda.synchronize()
+    return out
 
 
 def _bf16(bits):
@@ -190,3 +210,53 @@ def test_prefix_seeded_sweep(i):
     ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
                              case["scale"])
     parity.assert_parity(out, ref, what)
+
+
+@pytest.mark.parametrize("case_id", range(len(CASES)))
+@pytest.mark.parametrize("workers", [0, 1, 7, 1000])
+def test_prefix_fp8_matches_oracle(case_id, workers):
+    """sl_decode_attn_prefix_fp8: E4M3 pages with per-(page, KV head) scales, every row against
+    the oracle on the same codes and scales."""
+    members, prompts, gen, Hq, Hkv, D, extra = CASES[case_id]
+    what = f"fp8 case {case_id} workers {workers}"
+    print(what, flush=True)
+    rng = np.random.default_rng(60 + case_id)
+    b, starts, shared = grpo_fp8_batch(rng, members, prompts, gen, Hq, Hkv, D, extra, seed=70 + case_id)
+    out = run_prefix_fp8(b, starts, shared, workers)
+    parity.assert_parity(out, parity.oracle_full(b), what)
+
+
+def test_prefix_fp8_oversized_and_no_groups():
+    """E4M3 cache: a group too large for the 64 query rows and a group sharing nothing stay exact,
+    and no groups at all is plain attention."""
+    rng = np.random.default_rng(61)
+    b, starts, shared = grpo_fp8_batch(rng, [10, 3, 2], [48, 33, 5], 40, 28, 4, 128, seed=71)
+    parity.assert_parity(run_prefix_fp8(b, starts, shared), parity.oracle_full(b), "fp8 oversized group")
+    none_s = torch.zeros(1, dtype=torch.int32, device=DEV)
+    none_p = torch.zeros(0, dtype=torch.int32, device=DEV)
+    parity.assert_parity(run_prefix_fp8(b, none_s, none_p), parity.oracle_full(b), "fp8 no groups")
+
+
+def test_full_size_grpo_batch_fp8():
+    """32 prompts x 8 samples of 1024-token prompts over an E4M3 cache: sampled rows against the
+    oracle, and the whole output against the plain E4M3 kernel."""
+    b, starts, shared = inputs.make_grpo_batch(32, 8, 1024, seed=4, device=DEV, kv_dtype="e4m3")
+    torch.cuda.synchronize()
+    out = run_prefix_fp8(b, starts, shared)
+    rows = parity.sample_rows(b.seq_lens.cpu().numpy(), 24)
+    parity.assert_parity(out[rows], parity.oracle_rows(b, rows), "grpo fp8")
+    plain = sl.run_batch(b)
+    torch.cuda.synchronize()
+    assert (out.float() - plain.float()).abs().max().item() < 0.05
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_prefix_fp8_seeded_sweep(i):
+    members, prompts, gen, Hq, Hkv, D, extra, workers = _prefix_sweep_case(100 + i)
+    what = f"fp8 prefix sweep {i}: members={members} prompts={prompts} gen<={gen} Hq={Hq} Hkv={Hkv} D={D} " \
+           f"extra={extra} workers={workers}"
+    print(what, flush=True)
+    rng = np.random.default_rng(5000 + i)
+    b, starts, shared = grpo_fp8_batch(rng, members, prompts, gen, Hq, Hkv, D, extra, seed=5100 + i)
+    out = run_prefix_fp8(b, starts, shared, workers)
+    parity.assert_parity(out, parity.oracle_full(b), what)
