@@ -175,3 +175,43 @@ def test_engine_rejects_bad_arguments(lib):
     n = ctypes.c_int32(0)
     assert lib.sl_engine_run(None, 1, ctypes.byref(n)) == -1
     assert lib.sl_engine_destroy(None) == 0
+
+
+def _prefix(lib, d, fp8=False, q=FAKE, kp=FAKE, vp=FAKE, ks=FAKE, vs=FAKE, bt=FAKE, lens=FAKE, gs=FAKE, sp=FAKE,
+            ng=2, out=FAKE):
+    ref = ctypes.byref(d) if d is not None else None
+    if fp8:
+        return lib.sl_decode_attn_prefix_fp8(ref, q, kp, vp, ks, vs, bt, lens, gs, sp, ng, 0.125, out)
+    return lib.sl_decode_attn_prefix(ref, q, kp, vp, bt, lens, gs, sp, ng, 0.125, out)
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+def test_prefix_rejects_bad_arguments(lib, fp8):
+    """Prefix-shared attention validates before touching the GPU: nulls (the group arrays only when
+    there are groups, the scales only for E4M3), alignment, the group count, the batch limit and the
+    workspace; batch 0 is a no-op."""
+    d = _desc()
+    assert _prefix(lib, None, fp8) == -1
+    assert _prefix(lib, d, fp8, q=None) == -1
+    assert _prefix(lib, d, fp8, gs=None) == -1
+    assert _prefix(lib, d, fp8, sp=None) == -1
+    assert _prefix(lib, d, fp8, q=FAKE + 8) == -6
+    assert _prefix(lib, d, fp8, kp=FAKE + 2) == -6
+    assert _prefix(lib, d, fp8, gs=FAKE + 2) == -6
+    assert _prefix(lib, d, fp8, ng=-1) == -2
+    assert _prefix(lib, d, fp8, ng=5) == -2                  # more groups than sequences
+    assert _prefix(lib, _desc(batch=4097), fp8, ng=0) == -3
+    assert _prefix(lib, d, fp8, gs=None, sp=None, ng=0) == -4   # no groups: the arrays are not needed
+    assert _prefix(lib, d, fp8) == -4                        # valid arguments, no workspace
+    if fp8:
+        assert _prefix(lib, d, fp8, ks=None) == -1
+        assert _prefix(lib, d, fp8, vs=FAKE + 2) == -6
+    else:
+        assert _prefix(lib, d, fp8, ks=None, vs=None) == -4  # the bf16 call takes no scales
+    assert _prefix(lib, _desc(batch=0), fp8, q=None, kp=None, vp=None, ks=None, vs=None, bt=None, lens=None,
+                   gs=None, sp=None, ng=0, out=None) == 0
+    n0, n1 = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(d), 2, ctypes.byref(n0)) == 0
+    assert lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(d), 4, ctypes.byref(n1)) == 0
+    assert n1.value >= n0.value > 0
+    assert lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(d), 5, ctypes.byref(n0)) == -2

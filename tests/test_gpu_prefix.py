@@ -260,3 +260,13 @@ def test_prefix_fp8_seeded_sweep(i):
     b, starts, shared = grpo_fp8_batch(rng, members, prompts, gen, Hq, Hkv, D, extra, seed=5100 + i)
     out = run_prefix_fp8(b, starts, shared, workers)
     parity.assert_parity(out, parity.oracle_full(b), what)
+
+
+def test_max_prefix_batch_many_groups_fp8():
+    """The largest accepted batch (4096 sequences in 2048 groups of two) over an E4M3 cache, every row."""
+    rng = np.random.default_rng(55)
+    ng = 2048
+    b, starts, shared = grpo_fp8_batch(rng, [2] * ng, list(rng.integers(16, 49, ng)), 40, 8, 2, 64, seed=56)
+    assert b.seq_lens.shape[0] == 4096
+    print("fp8 batch 4096, 2048 groups", flush=True)
+    parity.assert_parity(run_prefix_fp8(b, starts, shared), parity.oracle_full(b), "fp8 batch 4096, 2048 groups")
