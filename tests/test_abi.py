@@ -215,3 +215,15 @@ def test_prefix_rejects_bad_arguments(lib, fp8):
     assert lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(d), 4, ctypes.byref(n1)) == 0
     assert n1.value >= n0.value > 0
     assert lib.sl_decode_attn_prefix_workspace_size(ctypes.byref(d), 5, ctypes.byref(n0)) == -2
+
+
+def test_missing_library_fails_loudly():
+    """Without the built library every entry point is unreachable: loading raises, there is no fallback."""
+    import subprocess
+    import sys
+    code = ("from paper_2504_15930_amd import sl\n"
+            "try:\n    sl.load('/nonexistent/libsl.so')\n"
+            "except ImportError as e:\n    print('ImportError', e)\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert "ImportError /nonexistent/libsl.so is missing" in r.stdout
