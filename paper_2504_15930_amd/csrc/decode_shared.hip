@@ -16,6 +16,10 @@
 // siblings find it in L2; no wavefront waits for another. Each wavefront
 // keeps one block's registers.
 //
+// The kernel is instantiated for bf16 and E4M3 pages. For E4M3 every
+// wavefront widens the whole shared tile itself (its block needs all keys and
+// values) and scales it by the page's own per-(page, KV head) scales.
+//
 // The own-page workgroups come first, so each CU holds one of them beside a
 // shared-page workgroup: the memory-bound and the MFMA-heavy pass share the
 // CUs instead of running one after the other.
