@@ -50,6 +50,20 @@ def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int,
     return kv + scales + qo + table
 
 
+def prefix_unique_bytes(seq_lens: np.ndarray, num_groups: int, shared_pages: int, num_q_heads: int,
+                        num_kv_heads: int, head_dim: int, kv_bytes: int, page_size: int = 16) -> int:
+    """Algorithmic bytes of prefix-shared attention when every sequence belongs to one of ``num_groups``
+    groups sharing ``shared_pages`` full pages: each shared page (its K and V rows, its table entry and,
+    for E4M3, its two scales) once per group, every own token and own page once, q and out."""
+    L = np.maximum(seq_lens.astype(np.int64), 0)
+    own_tokens = int((L - page_size * shared_pages).sum())
+    own_pages = int((-(-L // page_size) - shared_pages).sum())
+    pages = num_groups * shared_pages + own_pages
+    kv = (num_groups * shared_pages * page_size + own_tokens) * num_kv_heads * 2 * head_dim * kv_bytes
+    scales = pages * num_kv_heads * 2 * 4 if kv_bytes == 1 else 0
+    return kv + len(L) * 2 * num_q_heads * head_dim * 2 + pages * 4 + scales
+
+
 def append_bytes(seq_lens: np.ndarray, num_kv_heads: int, head_dim: int, kv_bytes: int) -> int:
     """Algorithmic bytes of one KV append: the new K and V rows (bf16) read, their cached form
     written, the per-(page, head) scales read and written (E4M3), and one length and one
@@ -201,12 +215,7 @@ def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
     Hq, Hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
     kvb = 1 if w.kv_dtype == "e4m3" else 2
     plain_bytes = algorithmic_bytes(L, Hq, Hkv, D, kvb)
-    sp = prompt_len // 16
-    own_tokens = int((L - 16 * sp).sum())
-    own_pages = int((-(-L // 16) - sp).sum())
-    pages = prompts * sp + own_pages
-    unique_bytes = ((prompts * sp * 16 + own_tokens) * Hkv * 2 * D * kvb + len(L) * 2 * Hq * D * 2
-                    + pages * 4 + (pages * Hkv * 2 * 4 if kvb == 1 else 0))
+    unique_bytes = prefix_unique_bytes(L, prompts, prompt_len // 16, Hq, Hkv, D, kvb)
     out = torch.empty_like(b.q)
 
     def plain():
