@@ -2,7 +2,7 @@
  * libsl skewness-aware dispatching: how many generation instances serve the
  * long-tail samples of a batch, and which instance receives each prompt.
  *
- * StreamRL Section 5.2 (Algorithm 2 with Equation 2). The prompts are sorted
+ * StreamRL Section 5.3, "Skewness-aware Scheduling" (Algorithm 2 with Equation 2). The prompts are sorted
  * by estimated output length, longest first, and the first
  * floor(alpha * num_prompts) of them are long-tail samples, the rest regular.
  * The P90 and P50 of a sample of output lengths stand for the average output

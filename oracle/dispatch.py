@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
 benchmark's ``cpu_baseline`` leg may import this module. Plain Python, written
 step by step from the algorithm.
 
-What it computes (Section 5.2, "Skewness-aware Scheduling"). A batch of
+What it computes (Section 5.3, "Skewness-aware Scheduling", the "Dispatching" part). A batch of
 prompts with estimated output lengths is to be spread over N generation
 instances. The prompts are sorted by estimate, longest first; the first
 alpha fraction are long-tail samples, the rest regular. The P90 and P50 of an
