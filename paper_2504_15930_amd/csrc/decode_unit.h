@@ -326,15 +326,31 @@ __device__ __forceinline__ void compute_tile(Piece<D> &st, const Tile<D, FP8> &t
 #pragma unroll
     for (int r = 0; r < 4; ++r)
         pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
-    const uint32_t p01 = pack_bf16(pr[0], pr[1]);
-    const uint32_t p23 = pack_bf16(pr[2], pr[3]);
-    st.l += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
+    // The value product takes the weights rounded to bf16, and the sum of
+    // weights adds those same rounded values, so the normalisation cancels
+    // their rounding: a token that holds all the weight returns its own value
+    // row exactly, and the remaining error scales with the spread of the value
+    // rows around the output. For E4M3 the weights carry the page's value
+    // scale, w = bf16(p s); the sum then adds w / s, the rounded weight without
+    // the scale (a zero or non-finite scale, for which that quotient is
+    // meaningless, adds the rounded p instead).
     i16x4_t pb;
     if constexpr (FP8) {
         const uint32_t w01 = pack_bf16(pr[0] * vmul, pr[1] * vmul);
         const uint32_t w23 = pack_bf16(pr[2] * vmul, pr[3] * vmul);
         pb = __builtin_bit_cast(i16x4_t, u32x2_t{w01, w23});
+        const float vinv = __builtin_amdgcn_rcpf(vmul);   // wave-uniform
+        if (__builtin_isfinite(vinv) && vinv != 0.0f) {
+            st.l += ((bf16_lo(w01) + bf16_hi(w01)) + (bf16_lo(w23) + bf16_hi(w23))) * vinv;
+        } else {
+            const uint32_t p01 = pack_bf16(pr[0], pr[1]);
+            const uint32_t p23 = pack_bf16(pr[2], pr[3]);
+            st.l += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
+        }
     } else {
+        const uint32_t p01 = pack_bf16(pr[0], pr[1]);
+        const uint32_t p23 = pack_bf16(pr[2], pr[3]);
+        st.l += (bf16_lo(p01) + bf16_hi(p01)) + (bf16_lo(p23) + bf16_hi(p23));
         pb = __builtin_bit_cast(i16x4_t, u32x2_t{p01, p23});
     }
 

@@ -10,21 +10,48 @@ import oracle
 # 1e-2 and relative 2e-2, applied per element as |gpu - ref| <= ATOL + RTOL |ref|
 # (the bf16 output alone is rounded by up to 2^-9 |ref|, which exceeds 1e-2 once
 # |ref| > 5, so a bare 1e-2 bound cannot hold for large outputs), and per
-# (sequence, head) row as ||gpu - ref||_2 <= RTOL ||ref||_2.
+# (sequence, head) row as ||gpu - ref||_2 <= RTOL ||ref||_2. Where |ref| < STRICT_BELOW
+# the bare absolute bound |gpu - ref| <= ATOL must hold as well: there the bf16
+# output rounding is at most half an ulp of [2, 4), 2^-7 = 7.8e-3, so the stated
+# 1e-2 is reachable, and the relative term cannot hide an arithmetic error of up
+# to 2-7x the stated bound for outputs of magnitude 0.5-3.
 ATOL = 1e-2
 RTOL = 2e-2
+STRICT_BELOW = 4.0
 
 
-def assert_parity(gpu: torch.Tensor, ref: np.ndarray, what: str = "", atol=ATOL, rtol=RTOL):
-    g = gpu.detach().float().cpu().double().numpy()
+def assert_parity(gpu, ref: np.ndarray, what: str = "", atol=ATOL, rtol=RTOL, strict_below=STRICT_BELOW,
+                  value_scale=None):
+    """Elementwise and row-wise parity of a bf16 GPU result with the fp64 oracle.
+
+    ``value_scale``: for inputs whose values are not of unit scale, the RMS of the cached value
+    rows each output row averages (array broadcastable to ref.shape[:-1] + (1,), see
+    ``value_rms_rows``). The absolute terms are stated for unit-scale data (the workloads draw
+    K and V from N(0, 1)); scaling V by s scales the output and every rounding error in it by s,
+    so there both the absolute bound and the |ref| range it covers are multiplied by max(1, s).
+    One such error is inherent to the method's arithmetic: softmax weights enter the value
+    product rounded to bf16 (relative error up to 2^-8 each), which moves the output by up to
+    2^-8 times the spread of the value rows around it, not of the output itself.
+    """
+    g = gpu.detach().float().cpu().double().numpy() if isinstance(gpu, torch.Tensor) else np.asarray(gpu, np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert g.shape == ref.shape, f"{what}: shape {g.shape} vs {ref.shape}"
     assert np.isfinite(g).all(), f"{what}: non-finite GPU output at {np.argwhere(~np.isfinite(g))[:5]}"
     err = np.abs(g - ref)
+    s = np.ones(ref.shape[:-1] + (1,)) if value_scale is None else np.maximum(1.0, np.asarray(value_scale, float))
+    s = np.broadcast_to(s, ref.shape)
+    atol = atol * s
+    strict_below = strict_below * s
     excess = err - (atol + rtol * np.abs(ref))
     worst = np.unravel_index(np.argmax(excess), err.shape)
-    assert excess.max() <= 0, (f"{what}: |err| {err[worst]:.3g} > {atol} + {rtol}|ref| "
+    assert excess.max() <= 0, (f"{what}: |err| {err[worst]:.3g} > {atol[worst]:.3g} + {rtol}|ref| "
                                f"(ref {ref[worst]:.3g}) at {worst}; max abs err {err.max():.3g}")
+    small = np.abs(ref) < strict_below
+    if small.any():
+        es = np.where(small, err - atol, -np.inf)
+        ws = np.unravel_index(np.argmax(es), err.shape)
+        assert es.max() <= 0, (f"{what}: |err| {err[ws]:.3g} > {atol[ws]:.3g} where |ref| < {strict_below[ws]:.3g} "
+                               f"(ref {ref[ws]:.3g}) at {ws}")
     num = np.sqrt(((g - ref) ** 2).sum(axis=-1))
     den = np.sqrt((ref ** 2).sum(axis=-1))
     zero = den == 0
@@ -32,6 +59,24 @@ def assert_parity(gpu: torch.Tensor, ref: np.ndarray, what: str = "", atol=ATOL,
     rel = num[~zero] / den[~zero]
     if rel.size:
         assert rel.max() <= rtol, f"{what}: max row relative L2 err {rel.max():.3g}"
+
+
+def value_rms_rows(v_pages: np.ndarray, block_table: np.ndarray, seq_lens: np.ndarray, num_q_heads: int):
+    """[B, Hq, 1]: RMS of the live cached value rows that each output row (sequence b, query head
+    h) averages, from float64 value pages [N, Hkv, P, D] (dequantised by the caller)."""
+    B = len(seq_lens)
+    N, Hkv, P, D = v_pages.shape
+    G = num_q_heads // Hkv
+    out = np.ones((B, num_q_heads, 1))
+    for b in range(B):
+        L = int(seq_lens[b])
+        if L <= 0:
+            continue
+        nb = -(-L // P)
+        rows = v_pages[block_table[b, :nb]].transpose(1, 0, 2, 3).reshape(Hkv, nb * P, D)[:, :L]
+        rms = np.sqrt((rows ** 2).mean(axis=(1, 2)))
+        out[b, :, 0] = np.repeat(rms, G)
+    return out
 
 
 def oracle_full(batch, threads: int = 0) -> np.ndarray:
