@@ -29,8 +29,10 @@ _LIBS: dict[str, ctypes.CDLL] = {}
 
 
 def load(path: str | None = None) -> ctypes.CDLL:
-    """Load (building first if absent) the oracle library at ``path``."""
-    path = path or _build.LIBRARY
+    """Load (building first if absent) the oracle library at ``path``; by default the one named
+    by the environment variable SL_ORACLE_LIBRARY (a build with the host sanitizers, say), else
+    the standard build."""
+    path = path or os.environ.get("SL_ORACLE_LIBRARY") or _build.LIBRARY
     lib = _LIBS.get(path)
     if lib is not None:
         return lib

@@ -19,6 +19,11 @@ CFLAGS = ["-std=c99", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fPIC",
           "-shared", "-fopenmp", "-Wall", "-Wextra"]
 
 
+# The host sanitizers, for a separate build of the oracle run under AddressSanitizer and
+# UndefinedBehaviorSanitizer by the sanitizer test.
+SANITIZE_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+
+
 def build(sources: str | list[str] | None = None, output: str = LIBRARY,
           extra: list[str] | None = None) -> str:
     """Compile ``sources`` (default: every oracle source) into the shared library

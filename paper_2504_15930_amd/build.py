@@ -60,5 +60,21 @@ def build(output: str = LIBRARY, extra: list[str] | None = None, verbose: bool =
     return output
 
 
+# Host-only build of the dispatching code (csrc/dispatch.cpp, no GPU code) with the host
+# sanitizers, loaded through SL_DISPATCH_LIBRARY by the sanitizer test.
+SANITIZE_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+
+
+def build_dispatch_host(output: str, extra: list[str] | None = None) -> str:
+    """Compile csrc/dispatch.cpp alone with the host C++ compiler into the shared library
+    ``output`` (the HIP headers are only read for the status type)."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["g++", "-std=c++17", "-O1", "-fPIC", "-shared", "-Wall", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(rocm, "include"), "-I", os.path.join(ROOT, "include"), *(extra or []),
+           os.path.join(CSRC, "dispatch.cpp"), "-o", output]
+    subprocess.run(cmd, check=True)
+    return output
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

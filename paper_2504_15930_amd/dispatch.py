@@ -6,6 +6,7 @@ this module converts numpy arrays and returns the plan.
 from __future__ import annotations
 
 import ctypes
+import os
 
 import numpy as np
 
@@ -16,8 +17,20 @@ class PtlProfile(ctypes.Structure):
     _fields_ = [("points", ctypes.c_int32), ("batch", ctypes.c_void_p), ("seconds", ctypes.c_void_p)]
 
 
+_host_lib: ctypes.CDLL | None = None
+
+
 def _lib():
-    lib = sl.load()
+    """libsl, or the host-only build of the dispatching code that the environment variable
+    SL_DISPATCH_LIBRARY names (``build.build_dispatch_host``, e.g. with the host sanitizers)."""
+    global _host_lib
+    path = os.environ.get("SL_DISPATCH_LIBRARY")
+    if path:
+        if _host_lib is None:
+            _host_lib = ctypes.CDLL(path)
+        lib = _host_lib
+    else:
+        lib = sl.load()
     if not getattr(lib, "_dispatch_typed", False):
         P = ctypes.c_void_p
         lib.sl_generation_latency.argtypes = [ctypes.POINTER(PtlProfile), ctypes.c_double, ctypes.c_int32,

@@ -17,5 +17,6 @@ def oracle_lib():
     """Path of the built oracle library (built once if absent)."""
     import oracle
     from oracle import build
-    oracle.load()
-    return build.LIBRARY
+    path = os.environ.get("SL_ORACLE_LIBRARY") or build.LIBRARY
+    oracle.load(path)
+    return path
