@@ -17,7 +17,13 @@ already resident in HBM. Prints one JSON line:
              taken on the current kernel source, else null;
   cpu_baseline  the fp64 CPU oracle timed on the host cores on a bounded
              sample of the same batch (the sequences and the byte count are
-             named in ``sample``); its outputs are also compared with the GPU's.
+             named in ``sample``); its outputs are also compared with the GPU's;
+             ``single_thread`` times it on one core over a 32-sequence subset;
+  configs    the other long-tail decode steps measured the same way in the
+             same run (straggler-only, 72B-like, E4M3 cache): step time, GB/s,
+             % of peak, steps/s, the split kernel's roofline and an oracle
+             baseline on a seeded subset of 32 sequences (always the longest
+             and the shortest) timed on all cores and on one.
 
 Single GPU only: ``--gpus`` above 1 exits with an explanation.
 """
@@ -37,6 +43,12 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "decode-attn achieved HBM GB/s (% of MI355X peak) + decode steps/s, long-tail batch"
 KERNEL_SOURCES = ["paper_2504_15930_amd/csrc/decode_split.hip", "paper_2504_15930_amd/csrc/decode_unit.h",
                   "paper_2504_15930_amd/csrc/sl_internal.h"]
+# Decode steps measured besides the headline one, with the share of peak HBM bandwidth each
+# one's step is to reach (None: reported only) and the layer count of the model whose heads it
+# has (Qwen2.5-7B: 28 layers, Qwen2.5-72B: 80), for attention-only steps/s of a whole model.
+OTHER_CONFIGS = ["straggler", "qwen72b_longtail", "fp8_qwen7b_longtail"]
+TARGET_PCT = {"qwen7b_longtail": 75.0, "qwen72b_longtail": 75.0, "straggler": 60.0, "fp8_qwen7b_longtail": None}
+MODEL_LAYERS = {"qwen7b_longtail": 28, "fp8_qwen7b_longtail": 28, "qwen72b_longtail": 80, "straggler": 80}
 
 
 def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int, head_dim: int,
@@ -293,70 +305,226 @@ def traffic_bytes(workload: str) -> float | None:
     return (fetch + write) * 1024.0
 
 
-def cpu_baseline(batch, out_gpu, target_s: float, threads: int = 0) -> dict:
-    """Time the oracle on a growing seeded sample of sequences until ~target_s of CPU work; when
-    the whole batch takes less than half of that, time repeated passes over it instead."""
+def compact_rows(batch, rows):
+    """Host copies of the inputs the oracle needs for sequences ``rows`` of a device batch: only
+    the pages they reference, compacted on the device and renumbered in their block-table rows,
+    so every cached token stays where the definition reads it."""
     import torch
 
+    L = batch.seq_lens.cpu().numpy()
+    bt = batch.block_table[list(rows)].cpu().numpy()
+    lens = L[list(rows)]
+    nb = -(-np.maximum(lens, 0) // 16)
+    used = np.unique(np.concatenate([bt[i, :nb[i]] for i in range(len(rows))]))
+    remap = np.zeros(int(used.max()) + 1, dtype=np.int32)
+    remap[used] = np.arange(len(used), dtype=np.int32)
+    new_bt = np.zeros_like(bt)
+    for i in range(len(rows)):
+        new_bt[i, :nb[i]] = remap[bt[i, :nb[i]]]
+    idx = torch.as_tensor(used.astype(np.int64), device=batch.k_pages.device)
+
+    def bits(t):
+        t = t.cpu().contiguous()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+    args = dict(q=bits(batch.q[list(rows)]), k_pages=bits(batch.k_pages.index_select(0, idx)),
+                v_pages=bits(batch.v_pages.index_select(0, idx)), block_table=new_bt, seq_lens=lens,
+                scale=batch.scale)
+    if batch.kv_dtype == "e4m3":
+        args["k_scales"] = batch.k_scales.index_select(0, idx).cpu().numpy()
+        args["v_scales"] = batch.v_scales.index_select(0, idx).cpu().numpy()
+    return args
+
+
+def parity_vs_gpu(out_gpu, rows, ref) -> dict:
+    g = out_gpu[list(rows)].float().cpu().double().numpy()
+    err = float(np.abs(g - ref).max())
+    rel = float((np.sqrt(((g - ref) ** 2).sum(-1)) / np.maximum(np.sqrt((ref ** 2).sum(-1)), 1e-30)).max())
+    return dict(max_abs_err=err, max_row_rel_l2=rel)
+
+
+def subset_rows(seq_lens: np.ndarray, n: int = 32, seed: int = 123) -> list[int]:
+    """n sequences of a batch (all of them if it has fewer): the longest and the shortest, the
+    rest a seeded random choice."""
+    L = np.asarray(seq_lens)
+    if len(L) <= n:
+        return list(range(len(L)))
+    pick = {int(np.argmax(L)), int(np.argmin(L))}
+    for i in np.random.default_rng(seed).permutation(len(L)):
+        if len(pick) >= n:
+            break
+        pick.add(int(i))
+    return sorted(pick)
+
+
+def oracle_timed(args, threads: int, passes: int = 1):
     import oracle
 
+    t0 = time.perf_counter()
+    for _ in range(passes):
+        ref = oracle.decode_attn(args["q"], args["k_pages"], args["v_pages"], args["block_table"],
+                                 args["seq_lens"], args["scale"], k_scales=args.get("k_scales"),
+                                 v_scales=args.get("v_scales"), threads=threads)
+    return ref, time.perf_counter() - t0
+
+
+def all_cores() -> int:
+    """Threads the oracle uses by default on this host (OpenMP's default, i.e. the cores this
+    process may run on unless OMP_NUM_THREADS says otherwise)."""
+    import oracle
+
+    return oracle.max_threads(0)
+
+
+def oracle_subset_baseline(batch, out_gpu, n: int = 32) -> dict:
+    """The oracle on a seeded subset of ``n`` sequences (always the longest and the shortest),
+    timed once on all cores and once on one core, in GB/s of the subset's algorithmic bytes."""
+    L = batch.seq_lens.cpu().numpy()
+    rows = subset_rows(L, n)
+    args = compact_rows(batch, rows)
+    Hq, D = batch.q.shape[1], batch.q.shape[2]
+    Hkv = batch.k_pages.shape[1]
+    kvb = 1 if batch.kv_dtype == "e4m3" else 2
+    nbytes = algorithmic_bytes(L[rows], Hq, Hkv, D, kvb)
+    cores = all_cores()
+    ref, dt = oracle_timed(args, cores)
+    ref1, dt1 = oracle_timed(args, 1)
+    sample = (f"{len(rows)} of {len(L)} sequences incl. the longest and the shortest ({int(L[rows].sum())} "
+              f"tokens, {nbytes / 1e6:.1f} MB algorithmic), seeded choice, 1 pass")
+    return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", cores=cores, kind="oracle", seconds=round(dt, 3),
+                sample=sample, parity_vs_gpu=parity_vs_gpu(out_gpu, rows, ref),
+                single_thread=dict(value=round(nbytes / dt1 / 1e9, 4), unit="GB/s", cores=1, seconds=round(dt1, 3),
+                                   sample=sample, same_result_as_all_cores=bool(np.array_equal(ref, ref1))))
+
+
+def cpu_baseline(batch, out_gpu, target_s: float) -> dict:
+    """Time the oracle on all cores on a growing seeded sample of sequences until ~target_s of CPU
+    work; when the whole batch takes less than half of that, time repeated passes over it instead.
+    ``single_thread``: the 32-sequence subset of ``oracle_subset_baseline`` on one core."""
     L = batch.seq_lens.cpu().numpy()
     order = list(np.random.default_rng(123).permutation(len(L)))
     Hq, D = batch.q.shape[1], batch.q.shape[2]
     Hkv = batch.k_pages.shape[1]
     kvb = 1 if batch.kv_dtype == "e4m3" else 2
-
-    def run(rows, passes=1):
-        bt = batch.block_table[rows].cpu().numpy()
-        lens = L[rows]
-        nb = -(-np.maximum(lens, 0) // 16)
-        used = np.unique(np.concatenate([bt[i, :nb[i]] for i in range(len(rows))]))
-        remap = np.zeros(int(used.max()) + 1, dtype=np.int32)
-        remap[used] = np.arange(len(used), dtype=np.int32)
-        new_bt = np.zeros_like(bt)
-        for i in range(len(rows)):
-            new_bt[i, :nb[i]] = remap[bt[i, :nb[i]]]
-        idx = torch.as_tensor(used.astype(np.int64), device=batch.k_pages.device)
-
-        def bits(t):
-            t = t.cpu().contiguous()
-            return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
-
-        args = dict(q=bits(batch.q[rows]), k_pages=bits(batch.k_pages.index_select(0, idx)),
-                    v_pages=bits(batch.v_pages.index_select(0, idx)))
-        kw = {}
-        if kvb == 1:
-            kw = dict(k_scales=batch.k_scales.index_select(0, idx).cpu().numpy(),
-                      v_scales=batch.v_scales.index_select(0, idx).cpu().numpy())
-        t0 = time.perf_counter()
-        for _ in range(passes):
-            ref = oracle.decode_attn(args["q"], args["k_pages"], args["v_pages"], new_bt, lens,
-                                     batch.scale, threads=threads, **kw)
-        return ref, time.perf_counter() - t0
+    cores = all_cores()
 
     n = 1
     rows = order[:n]
-    ref, dt = run(rows)
+    args = compact_rows(batch, rows)
+    ref, dt = oracle_timed(args, cores)
     while dt < target_s / 4 and n < len(L):
         rate = max(dt, 1e-3) / max(1, int(L[rows].sum()))
         want_tokens = target_s / rate
         cum = np.cumsum(L[order])
         n = int(min(len(L), max(n + 1, np.searchsorted(cum, want_tokens) + 1)))
         rows = order[:n]
-        ref, dt = run(rows)
+        args = compact_rows(batch, rows)
+        ref, dt = oracle_timed(args, cores)
     passes = 1
     if n == len(L) and dt < target_s / 2:   # the whole batch is quick: repeat it
         passes = max(2, int(round(target_s / max(dt, 1e-3))))
-        ref, dt = run(rows, passes)
+        ref, dt = oracle_timed(args, cores, passes)
     nbytes = algorithmic_bytes(L[rows], Hq, Hkv, D, kvb) * passes
-    g = out_gpu[rows].float().cpu().double().numpy()
-    err = float(np.abs(g - ref).max())
-    rel = float((np.sqrt(((g - ref) ** 2).sum(-1)) / np.maximum(np.sqrt((ref ** 2).sum(-1)), 1e-30)).max())
-    return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", cores=oracle.max_threads(threads),
+    sub = oracle_subset_baseline(batch, out_gpu)
+    return dict(value=round(nbytes / dt / 1e9, 4), unit="GB/s", cores=cores,
                 kind="oracle", seconds=round(dt, 3),
                 sample=f"{len(rows)} of {len(L)} sequences ({int(L[rows].sum())} tokens, "
                        f"{nbytes / passes / 1e6:.1f} MB algorithmic), seeded choice, {passes} pass(es)",
-                parity_vs_gpu=dict(max_abs_err=err, max_row_rel_l2=rel))
+                parity_vs_gpu=parity_vs_gpu(out_gpu, rows, ref),
+                single_thread=sub["single_thread"])
+
+
+def measure_attention(workload: str, batch, out, steps: int, warmup: int, workers: int) -> dict:
+    """Time ``steps`` whole decode-attention calls on ``batch`` (events around exactly those calls,
+    after ``warmup`` untimed ones), then the split-KV kernel alone over ``steps`` more calls (HIP
+    events the library records around it on its launch stream)."""
+    import torch
+
+    from paper_2504_15930_amd import inputs, sl
+
+    w = inputs.WORKLOADS[workload]
+    L = batch.seq_lens.cpu().numpy()
+    kvb = 1 if batch.kv_dtype == "e4m3" else 2
+    nbytes = algorithmic_bytes(L, w.num_q_heads, w.num_kv_heads, w.head_dim, kvb)
+    print(f"[bench] {workload}: warmup {warmup}", file=sys.stderr, flush=True)
+    for _ in range(warmup):
+        sl.run_batch(batch, out=out, num_workers=workers)
+    torch.cuda.synchronize()
+
+    # Pass A: exactly `steps` whole calls, bracketed by events on the stream and
+    # nothing else inside the timed region.
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    print(f"[bench] {workload}: timing {steps} steps", file=sys.stderr, flush=True)
+    wall0 = time.perf_counter()
+    t_all0.record()
+    for _ in range(steps):
+        sl.run_batch(batch, out=out, num_workers=workers)
+    t_all1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    # Pass B: the same calls again, each with HIP events that the library
+    # records around the split-KV kernel on its launch stream. The extra event
+    # records lengthen the step slightly, so this pass only supplies the
+    # kernel's duration.
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for e in starts + stops:
+        e.record()                          # creates the underlying hipEvent
+    t_b0 = torch.cuda.Event(enable_timing=True)
+    t_b1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    print(f"[bench] {workload}: timing {steps} split-KV kernels", file=sys.stderr, flush=True)
+    t_b0.record()
+    for i in range(steps):
+        sl.run_batch(batch, out=out, num_workers=workers, timing=(starts[i].cuda_event, stops[i].cuda_event))
+    t_b1.record()
+    torch.cuda.synchronize()
+
+    step_ms = t_all0.elapsed_time(t_all1) / steps
+    kern_ms = [a.elapsed_time(b) for a, b in zip(starts, stops)]
+    kern_avg = float(np.mean(kern_ms))
+    gbs = nbytes / (step_ms * 1e-3) / 1e9
+    achieved = nbytes / (kern_avg * 1e-3) / 1e9
+    nw = sl.num_workers(sl.make_desc(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, 16,
+                                     batch.block_table.shape[1], batch.k_pages.shape[0], workers), fp8=kvb == 1)
+    traffic = traffic_bytes(workload)
+    target = TARGET_PCT.get(workload)
+    return {
+        "ms_per_step": round(step_ms, 5),
+        "wall_ms_per_step": round(wall * 1e3 / steps, 5),
+        "GBps": round(gbs, 2),
+        "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2),
+        "steps_per_s": round(1e3 / step_ms, 2),
+        "model_layers": MODEL_LAYERS.get(workload),
+        "model_steps_per_s": round(1e3 / step_ms / MODEL_LAYERS[workload], 2) if workload in MODEL_LAYERS else None,
+        "target_pct_of_peak": target,
+        "meets_target": None if target is None else bool(100 * gbs / PEAK_HBM_GBS >= target),
+        "config": {
+            "workload": workload, "batch": w.batch, "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "page_size": 16,
+            "kv_dtype": batch.kv_dtype, "total_tokens": int(L.sum()), "max_seq_len": int(L.max()),
+            "algorithmic_bytes": nbytes, "workers": nw,
+        },
+        "roofline": {
+            "kernel": "split_kv_kernel",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "traffic_over_algorithmic": None if traffic is None else round(traffic / nbytes, 4),
+            "kernel_ms": round(kern_avg, 5),
+            "ms_per_step_with_kernel_events": round(t_b0.elapsed_time(t_b1) / steps, 5),
+            "kernel_ms_p10_p90": [round(float(np.percentile(kern_ms, 10)), 5),
+                                  round(float(np.percentile(kern_ms, 90)), 5)],
+            "algorithmic_bytes_per_launch": nbytes,
+            "kernel_source_sha": kernel_source_hash(),
+        },
+    }
 
 
 def main(argv=None) -> int:
@@ -368,7 +536,9 @@ def main(argv=None) -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workers", type=int, default=0, help="split-KV workers (0: library default)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="target CPU time of the oracle baseline (0 disables it)")
+                    help="target CPU time of the oracle baseline (0 disables every oracle timing)")
+    ap.add_argument("--configs", default=",".join(OTHER_CONFIGS),
+                    help="comma-separated workloads measured besides --workload ('' for none)")
     ap.add_argument("--generation", type=int, default=1,
                     help="also run a whole long-tail generation (decode engine, LPT vs FIFO admission); 0 skips it")
     ap.add_argument("--dispatch", type=int, default=1,
@@ -410,95 +580,31 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     L = batch.seq_lens.cpu().numpy()
     kvb = 1 if batch.kv_dtype == "e4m3" else 2
-    nbytes = algorithmic_bytes(L, w.num_q_heads, w.num_kv_heads, w.head_dim, kvb)
     out = torch.empty_like(batch.q)
-
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        sl.run_batch(batch, out=out, num_workers=args.workers)
-    torch.cuda.synchronize()
-
-    # Pass A (the headline): exactly `steps` whole calls, bracketed by events on
-    # the stream and nothing else inside the timed region.
-    t_all0 = torch.cuda.Event(enable_timing=True)
-    t_all1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    wall0 = time.perf_counter()
-    t_all0.record()
-    for i in range(args.steps):
-        sl.run_batch(batch, out=out, num_workers=args.workers)
-    t_all1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-
-    # Pass B (the roofline): the same calls again, each with HIP events that the
-    # library records around the split-KV kernel on its launch stream. The
-    # extra event records lengthen the step slightly, so this pass only
-    # supplies the kernel's duration.
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    for e in starts + stops:
-        e.record()                          # creates the underlying hipEvent
-    t_b0 = torch.cuda.Event(enable_timing=True)
-    t_b1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    print(f"[bench] timing {args.steps} split-KV kernels", file=sys.stderr, flush=True)
-    t_b0.record()
-    for i in range(args.steps):
-        sl.run_batch(batch, out=out, num_workers=args.workers,
-                     timing=(starts[i].cuda_event, stops[i].cuda_event))
-    t_b1.record()
-    torch.cuda.synchronize()
-
-    step_ms = t_all0.elapsed_time(t_all1) / args.steps
-    wall_ms = wall * 1e3 / args.steps
-    kern_ms = [s.elapsed_time(e) for s, e in zip(starts, stops)]
-    kern_avg = float(np.mean(kern_ms))
-    gbs = nbytes / (step_ms * 1e-3) / 1e9
-    achieved = nbytes / (kern_avg * 1e-3) / 1e9
-    workers = sl.num_workers(sl.make_desc(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, 16,
-                                          batch.block_table.shape[1], batch.k_pages.shape[0],
-                                          args.workers), fp8=kvb == 1)
+    head = measure_attention(args.workload, batch, out, args.steps, args.warmup, args.workers)
+    nbytes = head["config"]["algorithmic_bytes"]
     result = {
         "metric": METRIC,
-        "value": round(gbs, 2),
+        "value": head["GBps"],
         "unit": "GB/s",
-        "pct_of_peak": round(100 * gbs / PEAK_HBM_GBS, 2),
-        "steps_per_s": round(1e3 / step_ms, 2),
+        "pct_of_peak": head["pct_of_peak"],
+        "steps_per_s": head["steps_per_s"],
+        "model_steps_per_s": head["model_steps_per_s"],
+        "target_pct_of_peak": head["target_pct_of_peak"],
+        "meets_target": head["meets_target"],
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(step_ms, 5),
-        "wall_ms_per_step": round(wall_ms, 5),
+        "ms_per_step": head["ms_per_step"],
+        "wall_ms_per_step": head["wall_ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "e4m3" if kvb == 1 else "bf16",
         "accumulate": "f32",
         "data": "synthetic",
-        "config": {
-            "workload": args.workload,
-            "batch": w.batch, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
-            "head_dim": w.head_dim, "page_size": 16, "kv_dtype": batch.kv_dtype,
-            "total_tokens": int(L.sum()), "max_seq_len": int(L.max()),
-            "algorithmic_bytes": nbytes, "workers": workers, "seed": args.seed,
-        },
-        "roofline": {
-            "kernel": "split_kv_kernel",
-            "bound": "hbm",
-            "achieved": round(achieved, 2),
-            "peak": PEAK_HBM_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4),
-            "traffic": traffic_bytes(args.workload),
-            "kernel_ms": round(kern_avg, 5),
-            "ms_per_step_with_kernel_events": round(t_b0.elapsed_time(t_b1) / args.steps, 5),
-            "kernel_ms_p10_p90": [round(float(np.percentile(kern_ms, 10)), 5),
-                                  round(float(np.percentile(kern_ms, 90)), 5)],
-            "algorithmic_bytes_per_launch": nbytes,
-            "kernel_source_sha": kernel_source_hash(),
-        },
+        "config": dict(head["config"], seed=args.seed),
+        "roofline": head["roofline"],
     }
     # KV append (the step before attention) and the whole decode step (append +
     # attention). The new rows overwrite each sequence's newest slot, so
@@ -528,6 +634,10 @@ def main(argv=None) -> int:
     d1.record()
     torch.cuda.synchronize()
     decode_ms = d0.elapsed_time(d1) / args.steps
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for e in starts + stops:
+        e.record()
     for i in range(args.steps):
         append(timing=(starts[i].cuda_event, stops[i].cuda_event))
     torch.cuda.synchronize()
@@ -544,20 +654,42 @@ def main(argv=None) -> int:
         "steps_per_s": round(1e3 / decode_ms, 2),
         "GBps": round((nbytes + app_bytes) / (decode_ms * 1e-3) / 1e9, 2),
     }
+    if args.cpu_seconds > 0:
+        # The appends above rewrote each sequence's newest slot: run the step once more so the
+        # output the oracle is compared with belongs to the cache as it now stands.
+        sl.run_batch(batch, out=out, num_workers=args.workers)
+        torch.cuda.synchronize()
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(batch, out, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+
+    # The other decode steps, one batch resident at a time.
+    configs = [c for c in args.configs.split(",") if c and c != args.workload]
+    if configs:
+        del batch, out, k_new, v_new
+        torch.cuda.empty_cache()
+        result["configs"] = {}
+        for name in configs:
+            print(f"[bench] generating {name} (seed {args.seed})", file=sys.stderr, flush=True)
+            cb = inputs.make_batch(name, seed=args.seed, device=dev)
+            cout = torch.empty_like(cb.q)
+            torch.cuda.synchronize()
+            r = measure_attention(name, cb, cout, args.steps, args.warmup, args.workers)
+            if args.cpu_seconds > 0:
+                print(f"[bench] {name}: cpu baseline (oracle, subset)", file=sys.stderr, flush=True)
+                r["cpu_baseline"] = oracle_subset_baseline(cb, cout)
+            result["configs"][name] = r
+            del cb, cout
+            torch.cuda.empty_cache()
 
     if args.prefix:
         print("[bench] prefix sharing", file=sys.stderr, flush=True)
         result["prefix"] = prefix_experiment(w, args.seed, dev, args.steps, args.warmup)
     if args.generation:
-        result["generation"] = generation(w, batch.kv_dtype == "e4m3", args.seed, dev)
+        result["generation"] = generation(w, kvb == 1, args.seed, dev)
     if args.dispatch:
         result["dispatch"] = dispatch_experiment(w, args.seed, dev)
-
-    if args.cpu_seconds > 0:
-        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(batch, out, args.cpu_seconds)
-    else:
-        result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
     return 0
 

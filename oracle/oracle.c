@@ -189,13 +189,14 @@ int sl_oracle_decode_attn(int kv_kind, int B, int Hq, int Hkv, int D, int P,
             return -1;
 
 #ifdef _OPENMP
-    if (nthreads > 0)
-        omp_set_num_threads(nthreads);
+    /* The thread count applies to this call only (no global OpenMP setting). */
+    if (nthreads <= 0)
+        nthreads = omp_get_max_threads();
 #else
     (void)nthreads;
 #endif
     n = (long)nrows * Hq;
-#pragma omp parallel for schedule(dynamic, 1) reduction(min : status)
+#pragma omp parallel for schedule(dynamic, 1) reduction(min : status) num_threads(nthreads)
     for (i = 0; i < n; ++i) {
         int r = (int)(i / Hq);
         int h = (int)(i % Hq);
@@ -210,13 +211,11 @@ int sl_oracle_decode_attn(int kv_kind, int B, int Hq, int Hkv, int D, int P,
     return status;
 }
 
-/* Number of threads an OpenMP parallel region would use with this setting. */
+/* Number of threads sl_oracle_decode_attn uses for this setting. */
 int sl_oracle_max_threads(int nthreads)
 {
 #ifdef _OPENMP
-    if (nthreads > 0)
-        omp_set_num_threads(nthreads);
-    return omp_get_max_threads();
+    return nthreads > 0 ? nthreads : omp_get_max_threads();
 #else
     (void)nthreads;
     return 1;

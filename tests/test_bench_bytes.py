@@ -34,3 +34,12 @@ def test_prefix_unique_bytes_brute_force(kv, prompts, samples, prompt_len):
             + (pages * 2 * 2 * 4 if kvb == 1 else 0))
     assert bench.prefix_unique_bytes(L, prompts, prompt_len // 16, 8, 2, 64, kvb) == want
     assert bench.prefix_unique_bytes(L, prompts, 0, 8, 2, 64, kvb) == bench.algorithmic_bytes(L, 8, 2, 64, kvb)
+
+
+def test_subset_rows():
+    L = np.array([5, 90, 3, 40, 7, 1, 60, 8] * 10)
+    rows = bench.subset_rows(L, 32)
+    assert len(rows) == 32 and rows == sorted(set(rows))
+    assert int(np.argmax(L)) in rows and int(np.argmin(L)) in rows
+    assert bench.subset_rows(L[:20], 32) == list(range(20))
+    assert bench.subset_rows(L, 32) == rows   # seeded
