@@ -20,7 +20,8 @@ STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_U
                 -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
            "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_decode_attn_prefix",
-           "sl_decode_attn_prefix_fp8", "sl_decode_attn_prefix_workspace_size", "sl_status_string"]
+           "sl_decode_attn_prefix_fp8", "sl_decode_attn_prefix_workspace_size",
+           "sl_status_string"]
 # include/sl_engine.h (typed in engine.py)
 ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
 # include/sl_dispatch.h (typed in dispatch.py)
@@ -123,16 +124,21 @@ def num_workers(desc: Desc, fp8: bool = False) -> int:
     return n.value
 
 
-_workspaces: dict[int, torch.Tensor] = {}
+_workspaces: dict[tuple[int, int], torch.Tensor] = {}
 
 
 def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
-    """A cached per-device scratch buffer of at least ``nbytes`` (256-byte aligned by torch)."""
+    """A cached scratch buffer of at least ``nbytes`` (256-byte aligned by torch) per (device,
+    current stream). Calls on one stream run one after the other, so they may share a buffer;
+    calls on two streams could overlap, so each stream gets its own. The buffer is allocated
+    while its stream is current, so when it is replaced by a larger one torch's allocator hands
+    its memory out again only in that stream's order, after the kernels that used it."""
     idx = device.index if device.index is not None else torch.cuda.current_device()
-    ws = _workspaces.get(idx)
+    key = (idx, torch.cuda.current_stream(device).cuda_stream)
+    ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
-        _workspaces[idx] = ws
+        _workspaces[key] = ws
     return ws
 
 
