@@ -60,8 +60,10 @@ typedef enum sl_status {
     SL_ERR_UNSUPPORTED = -3, /* valid but not implemented: head_dim, page_size, group size, batch */
     SL_ERR_WORKSPACE = -4,   /* workspace NULL, too small or not 256-byte aligned */
     SL_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed */
-    SL_ERR_ALIGNMENT = -6    /* q, out or a page pool not 16-byte aligned; block_table,
+    SL_ERR_ALIGNMENT = -6,   /* q, out or a page pool not 16-byte aligned; block_table,
                                 seq_lens or a scale array not 4-byte aligned */
+    SL_ERR_SCRATCH_LIMIT = -7 /* sl_decode_attn_noalloc: the call needs more scratch than
+                                 SL_NOALLOC_SCRATCH_BYTES (use fewer workers) */
 } sl_status;
 
 /*
@@ -251,6 +253,29 @@ sl_status sl_kv_append_fp8(const sl_attn_desc *desc, const uint16_t *k_new, cons
                            const int32_t *block_table, const int32_t *seq_lens,
                            uint8_t *k_pages, uint8_t *v_pages, float *k_scales,
                            float *v_scales);
+
+/*
+ * Decode attention with a bf16 cache that allocates nothing, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc. Same arguments, kernels and result
+ * as sl_decode_attn (bit for bit, for the same worker count), except that
+ * desc->workspace and desc->workspace_bytes are ignored: the scratch lives in
+ * a fixed array of SL_NOALLOC_SCRATCH_BYTES inside the library, one per GPU,
+ * held until the process ends. The call makes no hipMalloc, hipFree or other
+ * allocating call. Calls on one GPU share that array: calls that overlap in
+ * time on one GPU (two streams, two threads) race and give undefined results;
+ * serialise them, e.g. on one stream. A call whose scratch (as
+ * sl_decode_attn_workspace_size would count it for its worker count) exceeds
+ * the array returns SL_ERR_SCRATCH_LIMIT before enqueuing anything; with the
+ * default worker count every supported shape fits.
+ * Errors: as sl_decode_attn, SL_ERR_WORKSPACE excepted, plus
+ * SL_ERR_SCRATCH_LIMIT.
+ */
+#define SL_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+sl_status sl_decode_attn_noalloc(const sl_attn_desc *desc, const uint16_t *q,
+                                 const uint16_t *k_pages, const uint16_t *v_pages,
+                                 const int32_t *block_table, const int32_t *seq_lens,
+                                 float scale, uint16_t *out);
 
 /* Static English description of a status code (never NULL). */
 const char *sl_status_string(sl_status status);

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIBRARY = os.path.join(HERE, "libsl.so")
 SOURCES = ["decode_split.hip", "decode_shared.hip", "merge.hip", "append.hip", "engine.hip", "api.cpp",
-           "engine.cpp", "dispatch.cpp"]
+           "engine.cpp", "dispatch.cpp", "noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -501,6 +501,7 @@ const char *sl_status_string(sl_status status)
     case SL_ERR_WORKSPACE: return "workspace missing, too small or not 256-byte aligned";
     case SL_ERR_HIP: return "HIP runtime call or kernel launch failed";
     case SL_ERR_ALIGNMENT: return "q, out or a page pool not 16-byte aligned, or an int/scale array not 4-byte aligned";
+    case SL_ERR_SCRATCH_LIMIT: return "the call needs more scratch than the allocation-free entry point's fixed array holds";
     }
     return "unknown status";
 }

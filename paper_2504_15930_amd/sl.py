@@ -17,10 +17,10 @@ LIBRARY = os.path.join(HERE, "libsl.so")
 
 SL_OK = 0
 STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_UNSUPPORTED",
-                -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT"}
+                -4: "SL_ERR_WORKSPACE", -5: "SL_ERR_HIP", -6: "SL_ERR_ALIGNMENT", -7: "SL_ERR_SCRATCH_LIMIT"}
 EXPORTS = ["sl_decode_attn_workspace_size", "sl_decode_attn_num_workers", "sl_decode_attn",
            "sl_decode_attn_fp8", "sl_kv_append", "sl_kv_append_fp8", "sl_decode_attn_prefix",
-           "sl_decode_attn_prefix_fp8", "sl_decode_attn_prefix_workspace_size",
+           "sl_decode_attn_prefix_fp8", "sl_decode_attn_prefix_workspace_size", "sl_decode_attn_noalloc",
            "sl_status_string"]
 # include/sl_engine.h (typed in engine.py)
 ENGINE_EXPORTS = ["sl_engine_create", "sl_engine_run", "sl_engine_schedule", "sl_engine_destroy"]
@@ -78,6 +78,7 @@ def load(path: str = LIBRARY) -> ctypes.CDLL:
     lib.sl_decode_attn_prefix_fp8.argtypes = [D, P, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_float, P]
     lib.sl_decode_attn_prefix_workspace_size.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
     lib.sl_kv_append_fp8.argtypes = [D, P, P, P, P, P, P, P, P]
+    lib.sl_decode_attn_noalloc.argtypes = [D, P, P, P, P, P, ctypes.c_float, P]
     lib.sl_status_string.argtypes = [ctypes.c_int]
     lib.sl_status_string.restype = ctypes.c_char_p
     for name in EXPORTS[:-1]:
@@ -215,6 +216,37 @@ def decode_attn(q, k_pages, v_pages, block_table, seq_lens, scale, *, out=None, 
     """
     return _run(False, q, k_pages, v_pages, None, None, block_table, seq_lens, scale, out,
                 num_workers, workspace, timing)
+
+
+def decode_attn_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, *, out=None,
+                        num_workers=0) -> torch.Tensor:
+    """``sl_decode_attn_noalloc``: ``sl_decode_attn`` with the library's fixed scratch array instead
+    of a workspace (the call allocates nothing). Calls on one GPU must not overlap in time."""
+    _need(q, "q", torch.bfloat16, 3)
+    _need(k_pages, "k_pages", torch.bfloat16, 4)
+    _need(v_pages, "v_pages", torch.bfloat16, 4)
+    _need(block_table, "block_table", torch.int32, 2)
+    _need(seq_lens, "seq_lens", torch.int32, 1)
+    B, Hq, D = q.shape
+    N, Hkv, P, D2 = k_pages.shape
+    if D2 != D or tuple(v_pages.shape) != tuple(k_pages.shape):
+        raise ValueError("q, k_pages and v_pages disagree on shape")
+    if block_table.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_table / seq_lens rows must equal the batch")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 3)
+        if out.shape != q.shape:
+            raise ValueError("out must have the shape of q")
+    with torch.cuda.device(q.device):
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+        desc = make_desc(B, Hq, Hkv, D, P, block_table.shape[1], N, num_workers, stream)
+        _check(load().sl_decode_attn_noalloc(ctypes.byref(desc), q.data_ptr(), k_pages.data_ptr(),
+                                             v_pages.data_ptr(), block_table.data_ptr(), seq_lens.data_ptr(),
+                                             float(scale), out.data_ptr()),
+               "sl_decode_attn_noalloc")
+    return out
 
 
 def decode_attn_fp8(q, k_pages, v_pages, k_scales, v_scales, block_table, seq_lens, scale, *,

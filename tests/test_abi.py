@@ -227,3 +227,16 @@ def test_missing_library_fails_loudly():
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr
     assert "ImportError /nonexistent/libsl.so is missing" in r.stdout
+
+
+def test_noalloc_host_checks(lib):
+    # Errors found on the host, before the fixed scratch array is looked up (no GPU needed).
+    assert lib.sl_decode_attn_noalloc(None, FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE) == -1
+    d = _desc(num_q_heads=7, num_kv_heads=2)
+    assert lib.sl_decode_attn_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE) == -2
+    # 65536 workers x 16 query heads x (128 + 2) floats x 2 slots: far beyond the fixed array
+    d = _desc(num_q_heads=32, num_kv_heads=2, num_workers=65536)
+    assert lib.sl_decode_attn_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE) == -7
+    assert "fixed array" in sl.status_string(-7)
+    d = _desc(batch=0)
+    assert lib.sl_decode_attn_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE) == 0
