@@ -125,19 +125,39 @@ def generation(w, fp8: bool, seed: int, dev) -> dict:
     return res
 
 
+def ptl_at(batch: int, prof_b, prof_s) -> float:
+    """PTL(batch) from a measured profile: linear between profiled batch sizes, the first value
+    below them, the last segment continued beyond them (as the dispatching code reads it)."""
+    xs, ys = list(prof_b), list(prof_s)
+    if batch <= xs[0] or len(xs) == 1:
+        return ys[0]
+    for k in range(1, len(xs)):
+        if batch <= xs[k]:
+            return ys[k - 1] + (ys[k] - ys[k - 1]) * (batch - xs[k - 1]) / (xs[k] - xs[k - 1])
+    return ys[-1] + (ys[-1] - ys[-2]) * (batch - xs[-1]) / (xs[-1] - xs[-2])
+
+
+DISPATCH_REGIMES = [(1024, 128), (1024, 32), (4096, 128)]   # (prompts, most sequences an instance decodes at once)
+
+
 def dispatch_experiment(w, seed: int, dev) -> dict:
-    """Skewness-aware dispatching (Algorithm 2) fed by PTL(BS) measured here, against random
-    dispatch, with the generation stage of each plan measured on the decode engine.
+    """Skewness-aware dispatching (Algorithm 2 with Equation 2) fed by PTL(BS) measured here,
+    against random dispatching, with the generation stage of every plan run on the decode engine.
 
     PTL(BS): one decode step (KV append + attention, this workload's heads) over BS sequences of
-    2048 cached tokens, for BS = 1 .. 256. Batch: 1024 prompts (256-768 tokens), true output
-    lengths lognormal (median 1024, sigma 1, capped at 8192), estimates = truth times a lognormal
-    error (sigma 0.3), the length distribution D a separate draw; N = 8 instances, alpha = 0.2,
-    at most 128 sequences per instance. An instance runs its samples on the engine (LPT inside).
-    Instances are independent, so the stage time of a plan is its most loaded instance: the
-    first instance of each group (it receives the longest sample of the group) for the
-    skewness-aware plans, the instances holding the longest sample and the most tokens for the
-    random one."""
+    2048 cached tokens, for BS = 1 .. 256. A batch of prompts (256-768 tokens) has true output
+    lengths lognormal (median 1024, sigma 1, capped at 8192); the estimates the dispatcher sees are
+    the truth times a lognormal error (sigma 0.3), standing in for the output-length ranker; the
+    length distribution D is a separate draw. N = 8 instances, alpha = 0.2. Three arms per regime:
+    random dispatch, skewness-aware dispatch on the noisy estimates, and skewness-aware dispatch on
+    the true lengths (the known-lengths setting). Every instance of every plan runs its prompts on
+    the engine (LPT admission by the arm's lengths, at most ``max_batch`` at once), and the stage
+    time of a plan is its slowest instance. Beside each measured stage: Equation 2's estimate for
+    the plan, and Sum over steps of PTL(sequences active in that step) along the slowest instance's
+    actual schedule. The regimes: 1024 prompts with 128 per instance at once (a random instance
+    holds 128 prompts: one round), and with 32 (four rounds), the case Equation 2's ceil(M / BS)
+    and the paper's scheduling-order discussion are about; and 4096 prompts with 128 at once (a
+    random instance holds 512 prompts: four rounds)."""
     import torch
 
     from paper_2504_15930_amd import dispatch as Dsp
@@ -164,47 +184,64 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
         prof_s.append(e0.elapsed_time(e1) / 30 * 1e-3)
         del b
         torch.cuda.empty_cache()
-    rng = np.random.default_rng(seed)
-    P, N, alpha, maxb = 1024, 8, 0.2, 128
-    true = np.clip(np.exp(rng.normal(np.log(1024), 1.0, P)), 16, 8192).astype(np.int32)
-    est = np.maximum(1, true * np.exp(rng.normal(0.0, 0.3, P))).astype(np.int32)
-    prompt = rng.integers(256, 769, P).astype(np.int32)
-    dist = np.clip(np.exp(rng.normal(np.log(1024), 1.0, 1024)), 16, 8192).astype(np.int32)
-
-    def run(sel):
-        idx = np.nonzero(sel)[0]
-        eng = E.Engine(prompt[idx], true[idx], est[idx], batch_slots=min(len(idx), maxb), num_q_heads=Hq,
-                       num_kv_heads=Hkv, head_dim=D, lpt=True, seed=seed, device=dev)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        eng.run()
-        e1.record()
-        torch.cuda.synchronize()
-        eng.close()
-        del eng
-        torch.cuda.empty_cache()
-        return round(e0.elapsed_time(e1), 2)
-
+    N, alpha = 8, 0.2
     res = {"ptl_profile": {"batch": prof_b, "us": [round(x * 1e6, 2) for x in prof_s],
                            "what": "KV append + decode attention, 2048 cached tokens per sequence"},
-           "prompts": P, "instances": N, "alpha": alpha, "max_batch": maxb}
-    measured = {}
-    for combine in ("sum", "max"):
-        print(f"[bench] dispatch plan ({combine})", file=sys.stderr, flush=True)
-        nl, nr, lat, inst = Dsp.plan(est, alpha, dist, N, prof_b, prof_s, maxb, combine)
-        if (nl, nr) not in measured:
-            measured[(nl, nr)] = max(run(inst == 0), run(inst == nl))
-        res[f"plan_{combine}"] = {"long_tail_instances": nl, "regular_instances": nr,
-                                  "estimated_ms": round(lat * 1e3, 2), "measured_stage_ms": measured[(nl, nr)]}
-    print("[bench] random dispatch", file=sys.stderr, flush=True)
-    perm = np.random.default_rng(seed + 1).permutation(P)
-    rinst = np.empty(P, np.int32)
-    rinst[perm] = np.arange(P) % N
-    worst = {max(range(N), key=lambda k: true[rinst == k].max()), max(range(N), key=lambda k: true[rinst == k].sum())}
-    res["random_stage_ms"] = max(run(rinst == k) for k in sorted(worst))
-    res["speedup_sum_plan"] = round(res["random_stage_ms"] / res["plan_sum"]["measured_stage_ms"], 3)
-    res["speedup_max_plan"] = round(res["random_stage_ms"] / res["plan_max"]["measured_stage_ms"], 3)
+           "instances": N, "alpha": alpha, "estimate_error_sigma": 0.3, "regimes": []}
+
+    for P, maxb in DISPATCH_REGIMES:
+        rng = np.random.default_rng(seed)
+        true = np.clip(np.exp(rng.normal(np.log(1024), 1.0, P)), 16, 8192).astype(np.int32)
+        est = np.maximum(1, true * np.exp(rng.normal(0.0, 0.3, P))).astype(np.int32)
+        prompt = rng.integers(256, 769, P).astype(np.int32)
+        dist = np.clip(np.exp(rng.normal(np.log(1024), 1.0, 1024)), 16, 8192).astype(np.int32)
+
+        def run_plan(inst, order_len):
+            """Every instance of a plan on the engine; its slowest instance is the stage time."""
+            per, sched = [], []
+            for k in range(N):
+                idx = np.nonzero(inst == k)[0]
+                if len(idx) == 0:
+                    per.append(0.0)
+                    sched.append(0.0)
+                    continue
+                eng = E.Engine(prompt[idx], true[idx], order_len[idx], batch_slots=min(len(idx), maxb),
+                               num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True, seed=seed, device=dev)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                eng.run()
+                e1.record()
+                torch.cuda.synchronize()
+                active = eng.schedule()[4]
+                per.append(round(e0.elapsed_time(e1), 2))
+                sched.append(round(1e3 * sum(ptl_at(int(a), prof_b, prof_s) for a in active), 2))
+                eng.close()
+                del eng
+                torch.cuda.empty_cache()
+            k = int(np.argmax(per))
+            return {"stage_ms": per[k], "instance_ms": per, "slowest_instance": k,
+                    "slowest_prompts": int((inst == k).sum()), "slowest_longest_output": int(true[inst == k].max()),
+                    "schedule_ptl_estimate_ms": sched[k]}
+
+        reg = {"prompts": P, "max_batch": maxb}
+        print(f"[bench] dispatch {P} prompts, {maxb} at once: random", file=sys.stderr, flush=True)
+        perm = np.random.default_rng(seed + 1).permutation(P)
+        rinst = np.empty(P, np.int32)
+        rinst[perm] = np.arange(P) % N
+        reg["random"] = run_plan(rinst, est)
+        for arm, lengths in (("skew_est", est), ("skew_true", true)):
+            done = {}
+            for combine in ("sum", "max"):
+                print(f"[bench] dispatch {P} prompts, {maxb} at once: {arm} ({combine})", file=sys.stderr, flush=True)
+                nl, nr, lat, inst = Dsp.plan(lengths, alpha, dist, N, prof_b, prof_s, maxb, combine)
+                if (nl, nr) not in done:
+                    done[(nl, nr)] = run_plan(inst, lengths)
+                r = dict(done[(nl, nr)])
+                r.update(long_tail_instances=nl, regular_instances=nr, eq2_estimate_ms=round(lat * 1e3, 2),
+                         speedup_over_random=round(reg["random"]["stage_ms"] / max(r["stage_ms"], 1e-9), 3))
+                reg[f"{arm}_{combine}"] = r
+        res["regimes"].append(reg)
     return res
 
 

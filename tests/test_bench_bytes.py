@@ -43,3 +43,12 @@ def test_subset_rows():
     assert int(np.argmax(L)) in rows and int(np.argmin(L)) in rows
     assert bench.subset_rows(L[:20], 32) == list(range(20))
     assert bench.subset_rows(L, 32) == rows   # seeded
+
+
+def test_ptl_at_hand_worked():
+    pb, ps = [1, 4, 8], [10.0, 16.0, 24.0]
+    assert bench.ptl_at(0, pb, ps) == 10.0 and bench.ptl_at(1, pb, ps) == 10.0   # flat below
+    assert bench.ptl_at(2, pb, ps) == 12.0                                       # 10 + 6 * 1/3
+    assert bench.ptl_at(6, pb, ps) == 20.0
+    assert bench.ptl_at(12, pb, ps) == 32.0                                      # last segment continued
+    assert bench.ptl_at(5, [3], [7.0]) == 7.0
