@@ -245,17 +245,24 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
     return res
 
 
-def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
-    """Prefix sharing on a GRPO-like batch with this workload's heads and cache type: 32 prompts
-    x 8 samples, 1024-token prompts (64 shared pages per group), generated lengths lognormal
+def prefix_subgroups(samples: int, group: int) -> int:
+    """Sub-groups a group of ``samples`` members is read as: one shared unit holds at most
+    min(16, 64 / G) members (64 query rows of G heads each)."""
+    return -(-samples // min(16, 64 // group))
+
+
+def prefix_experiment(w, seed: int, dev, steps: int, warmup: int, prompts: int = 32, samples: int = 8) -> dict:
+    """Prefix sharing on a GRPO-like batch with this workload's heads and cache type: ``prompts``
+    x ``samples``, 1024-token prompts (64 shared pages per group), generated lengths lognormal
     (median 512, sigma 1, capped at 4096). Plain decode attention reads every sample's copy of the
-    prompt pages; the prefix path reads each group's once. ``unique_bytes`` counts what the prefix
-    path has to read (shared pages and their scales once per group)."""
+    prompt pages; the prefix path reads them once per sub-group (a group larger than one shared
+    unit holds is read as several). ``unique_bytes`` counts what the prefix path has to read
+    (shared pages and their scales once per sub-group); ``ideal_bytes`` once per group."""
     import torch
 
     from paper_2504_15930_amd import inputs, sl
 
-    prompts, samples, prompt_len = 32, 8, 1024
+    prompt_len = 1024
     b, starts, shared = inputs.make_grpo_batch(prompts, samples, prompt_len, seed=seed + 11, device=dev,
                                                num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,
                                                head_dim=w.head_dim, kv_dtype=w.kv_dtype)
@@ -264,7 +271,9 @@ def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
     Hq, Hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
     kvb = 1 if w.kv_dtype == "e4m3" else 2
     plain_bytes = algorithmic_bytes(L, Hq, Hkv, D, kvb)
-    unique_bytes = prefix_unique_bytes(L, prompts, prompt_len // 16, Hq, Hkv, D, kvb)
+    subs = prefix_subgroups(samples, Hq // Hkv)
+    unique_bytes = prefix_unique_bytes(L, prompts * subs, prompt_len // 16, Hq, Hkv, D, kvb)
+    ideal_bytes = prefix_unique_bytes(L, prompts, prompt_len // 16, Hq, Hkv, D, kvb)
     out = torch.empty_like(b.q)
 
     def plain():
@@ -300,8 +309,10 @@ def prefix_experiment(w, seed: int, dev, steps: int, warmup: int) -> dict:
         "plain_ms": round(res["plain"], 5),
         "prefix_ms": round(res["prefix"], 5),
         "speedup": round(res["plain"] / res["prefix"], 3),
+        "subgroups_per_group": subs,
         "plain_bytes": plain_bytes,
         "unique_bytes": unique_bytes,
+        "ideal_bytes": ideal_bytes,
         "plain_GBps": round(plain_bytes / (res["plain"] * 1e-3) / 1e9, 2),
         "prefix_unique_GBps": round(unique_bytes / (res["prefix"] * 1e-3) / 1e9, 2),
         "prefix_effective_GBps": round(plain_bytes / (res["prefix"] * 1e-3) / 1e9, 2),
@@ -723,6 +734,8 @@ def main(argv=None) -> int:
     if args.prefix:
         print("[bench] prefix sharing", file=sys.stderr, flush=True)
         result["prefix"] = prefix_experiment(w, args.seed, dev, args.steps, args.warmup)
+        print("[bench] prefix sharing, 16 samples per prompt", file=sys.stderr, flush=True)
+        result["prefix_16"] = prefix_experiment(w, args.seed, dev, args.steps, args.warmup, prompts=16, samples=16)
     if args.generation:
         result["generation"] = generation(w, kvb == 1, args.seed, dev)
     if args.dispatch:

@@ -149,7 +149,8 @@ sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q,
 
 /*
  * Decode attention with prefix sharing (bf16 cache): the same result as
- * sl_decode_attn, reading each page that several sequences share only once.
+ * sl_decode_attn, reading each page that several sequences share only once
+ * per sub-group of at most min(16, 64 / (Hq / Hkv)) samples.
  * StreamRL's engine shares key-value cache between samples of one prompt
  * (Section 6, prefix sharing); here the samples of a group are run together
  * over the group's shared pages.
@@ -157,15 +158,20 @@ sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q,
  * Groups are runs of consecutive sequences: group k is sequences
  * [group_start[k], group_start[k+1]), and their first shared_pages[k] pages
  * are the same, i.e. block_table[b][i] == block_table[group_start[k]][i] for
- * i < shared_pages[k] and every member b (only the first member's entries are
- * read), and seq_lens[b] >= 16 * shared_pages[k]. Sequences in no group, or in
- * a group with shared_pages 0, are attended as by sl_decode_attn.
+ * i < shared_pages[k] and every member b (only the first member's entries of
+ * each sub-group are read), and seq_lens[b] >= 16 * shared_pages[k].
+ * Sequences in no group, or in a group with shared_pages 0, are attended as
+ * by sl_decode_attn.
  *   group_start   device int32 [num_groups + 1], ascending, within [0, batch]
  *   shared_pages  device int32 [num_groups]
  *   num_groups    0 .. batch (0: plain attention, in two passes)
- * A group with more than min(16, 64 / (Hq / Hkv)) members, or whose range or
- * page count is out of bounds, is treated as unshared (exact, without the
- * saving). A member shorter than its group's shared pages gets NaN rows.
+ * A group of m members with M = min(16, 64 / (Hq / Hkv)) is read as
+ * ceil(m / M) consecutive sub-groups of ceil(m / ceil(m / M)) members (the
+ * last may be smaller), each of which reads the shared pages once. A group
+ * that is empty, lies outside [0, batch], starts before the end of an earlier
+ * group's range (group_start not ascending), or whose page count lies outside
+ * 1 .. max_blocks_per_seq is treated as unshared (exact, without the saving).
+ * A member shorter than its group's shared pages gets NaN rows.
  * Everything else is as sl_decode_attn; batch is at most 4096, and the
  * workspace is sized by sl_decode_attn_prefix_workspace_size.
  * Errors: as sl_decode_attn (SL_ERR_SHAPE also for num_groups outside

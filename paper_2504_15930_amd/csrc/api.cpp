@@ -45,7 +45,8 @@ size_t prefix_workspace_layout(void *base, int batch, int max_blocks, int num_kv
     PrefixWorkspace w;
     w.cum_own = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)batch + 1)));
     w.seq_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4 * (size_t)batch));
-    w.cum_shared = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * ((size_t)num_groups + 1)));
+    w.cum_shared = reinterpret_cast<int32_t *>(
+        take(sizeof(int32_t) * ((size_t)prefix_max_sub(batch, num_groups, group) + 1)));
     w.own_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * 2));
     w.own_acc = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * group * head_dim));
     w.shared_ml = reinterpret_cast<float *>(take(sizeof(float) * 2 * (size_t)num_workers * kPrefixRows * 2));
@@ -335,6 +336,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const void *k_pag
     pp.cum_shared = ws.cum_shared;
     pp.seq_shared = ws.seq_shared;
     pp.num_groups = num_groups;
+    pp.max_sub = prefix_max_sub(d->batch, num_groups, G);
 
     SplitParams sp_;
     sp_.q = q;
@@ -394,7 +396,7 @@ sl_status run_prefix(const sl_attn_desc *d, const uint16_t *q, const void *k_pag
     mp.shared_unit_acc = ws.shared_unit_acc;
     mp.out = out;
     mp.batch = d->batch;
-    mp.num_groups = num_groups;
+    mp.max_sub = pp.max_sub;
     mp.num_q_heads = d->num_q_heads;
     mp.num_kv_heads = d->num_kv_heads;
     mp.group = G;

@@ -454,9 +454,20 @@ __device__ __forceinline__ void finish_unit(const SplitParams &p, Piece<D> &st, 
     }
 }
 
+struct ScanSum {
+    static constexpr int32_t kIdentity = 0;
+    __device__ static int32_t op(int32_t a, int32_t b) { return a + b; }
+};
+struct ScanMax {
+    static constexpr int32_t kIdentity = -2147483647 - 1;
+    __device__ static int32_t op(int32_t a, int32_t b) { return a > b ? a : b; }
+};
+
 // Turns a[0, n) (in LDS, written before a barrier) into its exclusive
-// prefix sum and stores the total in a[n]. Every thread of the workgroup
-// calls it; each scans a contiguous run. Ends with a barrier.
+// prefix scan under Op (sum or maximum) and stores the total in a[n]. Every
+// thread of the workgroup calls it; each scans a contiguous run. Ends with a
+// barrier.
+template <class Op = ScanSum>
 __device__ __forceinline__ void block_exclusive_scan(int32_t *a, int n)
 {
     __shared__ int32_t s_wave[kWavesPerBlock];
@@ -464,31 +475,33 @@ __device__ __forceinline__ void block_exclusive_scan(int32_t *a, int n)
     const int tid = threadIdx.x;
     const int per = (n + T - 1) / T;
     const int lo = min(n, tid * per), hi = min(n, lo + per);
-    int local = 0;
+    int local = Op::kIdentity;
     for (int i = lo; i < hi; ++i)
-        local += a[i];
+        local = Op::op(local, a[i]);
     const int lane = tid & (kWave - 1), wave = tid / kWave;
     int incl = local;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
         const int v = __shfl_up(incl, off, kWave);
         if (lane >= off)
-            incl += v;
+            incl = Op::op(incl, v);
     }
+    const int excl_in_wave = __shfl_up(incl, 1, kWave);
     if (lane == kWave - 1)
         s_wave[wave] = incl;
     __syncthreads();
-    int base = 0, total = 0;
+    int base = Op::kIdentity, total = Op::kIdentity;
 #pragma unroll
     for (int k = 0; k < kWavesPerBlock; ++k) {
-        base += k < wave ? s_wave[k] : 0;
-        total += s_wave[k];
+        if (k < wave)
+            base = Op::op(base, s_wave[k]);
+        total = Op::op(total, s_wave[k]);
     }
-    int run = base + incl - local;
+    int run = Op::op(base, lane > 0 ? excl_in_wave : Op::kIdentity);
     for (int i = lo; i < hi; ++i) {
         const int v = a[i];
         a[i] = run;
-        run += v;
+        run = Op::op(run, v);
     }
     if (tid == 0)
         a[n] = total;

@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p, int
 }
 
 // Prefix-sharing mode: every (sequence, head) row with shared pages, or whose
-// own pages were cut across workers, combines the pieces of its group's
+// own pages were cut across workers, combines the pieces of its sub-group's
 // shared unit (row member * G + head of the shared partial states) with the
 // pieces of its own unit. A unit cut across workers left one piece per worker
 // in the worker slots; a unit that one worker saw whole left its state in the
@@ -224,7 +224,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_prefix_kernel(PrefixMerge
     const int co = p.cum_own[b];
     const int ob = p.cum_own[b + 1] - co;
     const long long tot_o = (long long)p.cum_own[p.batch] * Hkv;
-    const long long tot_s = (long long)p.cum_shared[p.num_groups] * Hkv;
+    const long long tot_s = (long long)p.cum_shared[p.max_sub] * Hkv;
     const bool bad = L < 0 || L > p.max_blocks * kPageSize || L < sk * kPageSize;
     if (sk == 0 && ob == 0) {
         const uint16_t fill = L < 0 ? 0x7fc0 : 0x0000;   // bf16 NaN / +0

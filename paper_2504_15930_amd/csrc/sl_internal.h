@@ -140,11 +140,27 @@ struct PrefixParams {
     const int32_t *group_start;   // [num_groups + 1]
     const int32_t *shared_pages;  // [num_groups]
     int32_t *cum_own;             // [B + 1] prefix sum of own (unshared) pages
-    int32_t *cum_shared;          // [num_groups + 1] prefix sum of shared pages
-    int32_t *seq_shared;          // [B][4] per sequence: first shared page of its group in the shared
-                                  // stream, shared pages, group's first member, group (-1, zeros if unshared)
+    int32_t *cum_shared;          // [max_sub + 1] prefix sum of shared pages per sub-group
+    int32_t *seq_shared;          // [B][4] per sequence: first shared page of its sub-group in the shared
+                                  // stream, shared pages, sub-group's first member, sub-group (-1, zeros if
+                                  // unshared)
     int32_t num_groups;
+    int32_t max_sub;              // prefix_max_sub: bound on the sub-groups (shared-stream "sequences")
 };
+
+// Members of one shared unit: as many samples as fit kPrefixRows query rows,
+// at most 16 (the tile metadata keeps members - 1 in four bits).
+__host__ __device__ inline int prefix_max_members(int group) { return 16 < kPrefixRows / group ? 16 : kPrefixRows / group; }
+// Bound on the sub-groups of a call: shared groups are disjoint ranges of the
+// batch and a group of m members is cut into ceil(m / M) sub-groups, so there
+// are at most num_groups + batch / M of them, and never more than batch.
+__host__ __device__ inline int prefix_max_sub(int batch, int num_groups, int group)
+{
+    if (num_groups <= 0)
+        return 0;
+    const int bound = num_groups + batch / prefix_max_members(group);
+    return bound < batch ? bound : batch;
+}
 
 struct PrefixMergeParams {
     const int32_t *seq_lens;
@@ -158,7 +174,7 @@ struct PrefixMergeParams {
     const float *own_unit_ml, *own_unit_acc;        // [B Hkv][G][2 | D]: whole own units
     const float *shared_unit_ml, *shared_unit_acc;  // [B Hkv][kPrefixRows][2 | D]: whole shared units
     uint16_t *out;
-    int32_t batch, num_groups, num_q_heads, num_kv_heads, group, num_workers, max_blocks;
+    int32_t batch, max_sub, num_q_heads, num_kv_heads, group, num_workers, max_blocks;
     int32_t num_shared_workers;   // base and largest count of shared-page workgroups
     int32_t max_shared_workers;   // (effective_shared_workers)
 };
@@ -220,11 +236,11 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
 // lengths (B ints).
 inline size_t split_dynamic_lds(int batch) { return sizeof(int32_t) * (2 * (size_t)batch + 1); }
 // The fused prefix kernel's: for the sequences the own-page prefix sum, the
-// lengths and the groups (3 B + 1 ints), for the groups the shared-page prefix
-// sum and the packed first member and size (2 NG + 1 ints).
-inline size_t prefix_dynamic_lds(int batch, int num_groups)
+// sub-groups and the lengths (3 B + 2 ints), for the sub-groups the
+// shared-page prefix sum and the packed first member and size (2 S + 1 ints).
+inline size_t prefix_dynamic_lds(int batch, int max_sub)
 {
-    return sizeof(int32_t) * (3 * (size_t)batch + 2 * (size_t)num_groups + 2);
+    return sizeof(int32_t) * (3 * (size_t)batch + 2 * (size_t)max_sub + 3);
 }
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Prefix mode: the own-page pass (single-unit workers) and the shared-page

@@ -52,3 +52,9 @@ def test_ptl_at_hand_worked():
     assert bench.ptl_at(6, pb, ps) == 20.0
     assert bench.ptl_at(12, pb, ps) == 32.0                                      # last segment continued
     assert bench.ptl_at(5, [3], [7.0]) == 7.0
+
+
+def test_prefix_subgroups():
+    assert bench.prefix_subgroups(8, 7) == 1 and bench.prefix_subgroups(16, 7) == 2   # M = 9
+    assert bench.prefix_subgroups(20, 7) == 3 and bench.prefix_subgroups(16, 4) == 1  # M = 16
+    assert bench.prefix_subgroups(33, 8) == 5 and bench.prefix_subgroups(1, 16) == 1  # M = 8, 4

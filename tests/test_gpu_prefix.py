@@ -113,8 +113,8 @@ def test_no_groups_is_plain_attention():
 
 
 def test_oversized_and_zero_share_groups_stay_exact():
-    """A group with more members than fit the 64 query rows, and groups sharing no page, are
-    attended without sharing."""
+    """A group with more members than fit the 64 query rows (read as sub-groups), and groups
+    sharing no page (attended without sharing), stay exact."""
     rng = np.random.default_rng(51)
     case, starts, shared = grpo_case(rng, [10, 3, 2], [48, 33, 5], 40, 28, 4, 128)   # 10 * 7 = 70 > 64 rows
     out = run_prefix(case, starts, shared)
@@ -270,3 +270,74 @@ def test_max_prefix_batch_many_groups_fp8():
     assert b.seq_lens.shape[0] == 4096
     print("fp8 batch 4096, 2048 groups", flush=True)
     parity.assert_parity(run_prefix_fp8(b, starts, shared), parity.oracle_full(b), "fp8 batch 4096, 2048 groups")
+
+
+SPLIT_CASES = [
+    # members, prompt lengths, max generated, Hq, Hkv, D, extra: groups beyond M = min(16, 64 / G)
+    ([16, 20, 9, 1], [300, 64, 100, 48], 60, 28, 4, 128, 2),   # G = 7, M = 9: 8+8, 7+7+6, 9, 1
+    ([40, 17], [130, 16], 30, 16, 16, 64, 0),                  # G = 1, M = 16: 14+14+12, 9+8
+    ([33], [200], 10, 64, 8, 128, 1),                          # G = 8, M = 8: 7+7+7+7+5
+]
+
+
+@pytest.mark.parametrize("case_id", range(len(SPLIT_CASES)))
+@pytest.mark.parametrize("workers", [0, 1, 7, 1000])
+def test_large_groups_split_into_subgroups(case_id, workers):
+    """Groups with more members than one shared unit holds are read as consecutive sub-groups,
+    each over the shared pages once: every row against the oracle."""
+    members, prompts, gen, Hq, Hkv, D, extra = SPLIT_CASES[case_id]
+    what = f"split case {case_id} workers {workers}"
+    print(what, flush=True)
+    rng = np.random.default_rng(90 + case_id)
+    case, starts, shared = grpo_case(rng, members, prompts, gen, Hq, Hkv, D, extra)
+    out = run_prefix(case, starts, shared, workers)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, what)
+
+
+def test_whole_batch_one_group():
+    """All 300 sequences in one group (G = 4, M = 16: 18 sub-groups of 16 and one of 12)."""
+    rng = np.random.default_rng(95)
+    case, starts, shared = grpo_case(rng, [300], [520], 40, 16, 4, 128)
+    out = run_prefix(case, starts, shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "one group of 300")
+
+
+def test_non_ascending_group_start_stays_exact():
+    """group_start [0, 4, 0, 2, 7]: group 1 is empty (4 > 0), group 2 ([0, 2)) starts before the end
+    of group 0 ([0, 4)) and overlaps it, so it must not be shared (sharing both would let two
+    shared units claim the same sequences); group 3 ([2, 7)) overlaps group 0 too. Only group 0 is
+    shared; every row stays exact."""
+    rng = np.random.default_rng(96)
+    case, starts, shared = grpo_case(rng, [4, 3], [96, 40], 30, 28, 4, 128, extra=2)
+    bad_starts = np.array([0, 4, 0, 2, 7], np.int32)
+    bad_shared = np.array([shared[0], 1, 2, 1], np.int32)
+    out = run_prefix(case, bad_starts, bad_shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "non-ascending group_start")
+    for workers in (1, 1000):
+        parity.assert_parity(run_prefix(case, bad_starts, bad_shared, workers), ref, f"non-ascending w={workers}")
+
+
+def test_large_groups_split_fp8():
+    """E4M3 cache: the first split case (16, 20, 9, 1 members at G = 7), every row against the oracle."""
+    members, prompts, gen, Hq, Hkv, D, extra = SPLIT_CASES[0]
+    rng = np.random.default_rng(97)
+    b, starts, shared = grpo_fp8_batch(rng, members, prompts, gen, Hq, Hkv, D, extra, seed=98)
+    for workers in (0, 7):
+        parity.assert_parity(run_prefix_fp8(b, starts, shared, workers), parity.oracle_full(b),
+                             f"fp8 split workers={workers}")
+
+
+def test_max_prefix_batch_one_group():
+    """The largest accepted batch (4096 sequences) as one group: 256 sub-groups of 16 (G = 4)."""
+    rng = np.random.default_rng(99)
+    case, starts, shared = grpo_case(rng, [4096], [40], 20, 8, 2, 64)
+    out = run_prefix(case, starts, shared)
+    ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
+                             case["scale"])
+    parity.assert_parity(out, ref, "batch 4096, one group")
