@@ -463,6 +463,58 @@ struct ScanMax {
     __device__ static int32_t op(int32_t a, int32_t b) { return a > b ? a : b; }
 };
 
+// Output staging for plain attention. Vector-memory stores and loads share
+// one completion counter on this part, so a wait for a load issued after a
+// store also waits for the store, which under a full read stream takes
+// microseconds: writing each finished unit's rows out at once stalled the
+// worker at its next tile (measured: 3.4 us per unit with 256-token
+// sequences, the whole-kernel rate 5.5 instead of 6.8 TB/s). Finished rows are
+// therefore normalised into a per-wave LDS stage and written out only when
+// the stage is full or the worker's range ends, where no later load waits on
+// them.
+constexpr int kOutStageBytes = 16384;                       // per wave
+constexpr int kMaxOutSlots = kOutStageBytes / (1 * 64 * 2); // smallest slot: G = 1, D = 64
+
+// The bf16 rows of a finished unit (this lane's D/4 outputs of row n) into
+// its stage slot; l is the head's full sum of weights.
+template <int D>
+__device__ __forceinline__ void stage_output(const Piece<D> &st, float l, bool bad, uint8_t *slot, int n, int quad)
+{
+    const float inv = bad ? __builtin_nanf("") : 1.0f / l;
+    uint8_t *dst = slot + ((size_t)n * D + quad * (D / 4)) * 2;
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int k0 = 8 * c + 2 * e;   // flat index r * (D/16) + i, as in finish_unit
+            const int r0 = k0 / (D / 16), i0 = k0 % (D / 16);
+            const int k1 = k0 + 1;
+            const int r1 = k1 / (D / 16), i1 = k1 % (D / 16);
+            wv[e] = pack_bf16(st.acc[i0][r0] * inv, st.acc[i1][r1] * inv);
+        }
+        *reinterpret_cast<u32x4_t *>(dst + 16 * c) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
+    }
+}
+
+// Write the first `count` staged units out. A unit's G rows are one
+// contiguous block of G * D * 2 bytes both in the stage and in `out` (from
+// row rows[s]), so every lane copies 16-byte pieces 1 KB apart: each store
+// instruction writes whole cache lines. (Stored straight from the
+// accumulator layout, each instruction left 16-byte pieces 64 bytes apart,
+// over a hundred partial-line writes per unit, which drained slowly enough
+// under a full read stream to cost ~20 us per flush of nine units.)
+__device__ __forceinline__ void flush_outputs(const SplitParams &p, int head_dim, const uint8_t *stage,
+                                              const uint32_t *rows, int count, int slot_bytes, int lane)
+{
+    for (int s = 0; s < count; ++s) {
+        const uint8_t *src = stage + (size_t)s * slot_bytes;
+        uint8_t *dst = reinterpret_cast<uint8_t *>(p.out + (size_t)rows[s] * head_dim);
+        for (int off = 16 * lane; off < slot_bytes; off += 16 * kWave)
+            *reinterpret_cast<u32x4_t *>(dst + off) = *reinterpret_cast<const u32x4_t *>(src + off);
+    }
+}
+
 // Turns a[0, n) (in LDS, written before a barrier) into its exclusive
 // prefix scan under Op (sum or maximum) and stores the total in a[n]. Every
 // thread of the workgroup calls it; each scans a contiguous run. Ends with a
@@ -583,6 +635,16 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
     __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    // Plain attention: per-wave stage of finished units' output rows (see
+    // stage_output), `staged` of them queued, each slot G rows of D bf16.
+    constexpr bool kStageOut = MODE == kAllPages;
+    __shared__ uint8_t out_stage[kWavesPerBlock][kStageOut ? kOutStageBytes : 16];
+    __shared__ uint32_t out_rows[kWavesPerBlock][kStageOut ? kMaxOutSlots : 1];
+    uint8_t *const ostage = out_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    uint32_t *const orows = out_rows[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    const int slot_bytes = G * D * 2;
+    const int out_slots = kOutStageBytes / slot_bytes;   // >= 4 (G <= 16, D <= 128)
+    int staged = 0;
 
     // Tile entries, fetched in tile order (every call below asks for the next
     // tile; past the range the last tile repeats): {block-table entry (loaded
@@ -749,7 +811,19 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
                     float *const pml = to_unit ? p.unit_ml : p.part_ml;
                     float *const pacc = to_unit ? p.unit_acc : p.part_acc;
                     const size_t slot = to_unit ? (size_t)(row0 / (uint32_t)G) : 2 * (size_t)w + slot_sel;
-                    finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
+                    if (kStageOut && whole) {
+                        const float l = quad_sum(st.l);
+                        if (n < G)
+                            stage_output<D>(st, l, bad, ostage + (size_t)staged * slot_bytes, n, quad);
+                        if (lane == 0)
+                            orows[staged] = row0;
+                        if (++staged == out_slots) {
+                            flush_outputs(p, D, ostage, orows, staged, slot_bytes, lane);
+                            staged = 0;
+                        }
+                    } else {
+                        finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
+                    }
                     reset(st);
                     started = false;
                     bad = false;
@@ -758,6 +832,8 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
             }
         }
     }
+    if (kStageOut && staged > 0)
+        flush_outputs(p, D, ostage, orows, staged, slot_bytes, lane);
 }
 
 }  // namespace
