@@ -467,11 +467,12 @@ struct ScanMax {
 // one completion counter on this part, so a wait for a load issued after a
 // store also waits for the store, which under a full read stream takes
 // microseconds: writing each finished unit's rows out at once stalled the
-// worker at its next tile (measured: 3.4 us per unit with 256-token
-// sequences, the whole-kernel rate 5.5 instead of 6.8 TB/s). Finished rows are
-// therefore normalised into a per-wave LDS stage and written out only when
-// the stage is full or the worker's range ends, where no later load waits on
-// them.
+// worker at its next tile (measured: ~2.9 us per unit with 256-token
+// sequences), and so did the partial state of the range's first, cut unit
+// (2.6% of the 7B-like step). Finished rows are therefore normalised into a
+// per-wave LDS stage, and the first piece's state kept there too, and both
+// are written out only when the stage is full or the worker's range ends,
+// where no later load waits on them.
 constexpr int kOutStageBytes = 16384;                       // per wave
 constexpr int kMaxOutSlots = kOutStageBytes / (1 * 64 * 2); // smallest slot: G = 1, D = 64
 
@@ -513,6 +514,41 @@ __device__ __forceinline__ void flush_outputs(const SplitParams &p, int head_dim
         for (int off = 16 * lane; off < slot_bytes; off += 16 * kWave)
             *reinterpret_cast<u32x4_t *>(dst + off) = *reinterpret_cast<const u32x4_t *>(src + off);
     }
+}
+
+// The partial state (m, l, acc) of a cut unit into the stage, laid out as
+// in the workspace: G rows of D fp32 (acc), then G pairs (m, l); l is the
+// head's full sum of weights.
+template <int D>
+__device__ __forceinline__ void stage_partial(const Piece<D> &st, float l, bool bad, uint8_t *area, int G, int n,
+                                              int quad)
+{
+    const float poison = bad ? __builtin_nanf("") : 0.0f;
+    float *acc = reinterpret_cast<float *>(area) + (size_t)n * D + quad * (D / 4);
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < D / 16; i += 4)
+            *reinterpret_cast<f32x4_t *>(acc + r * (D / 16) + i) =
+                f32x4_t{st.acc[i][r], st.acc[i + 1][r], st.acc[i + 2][r], st.acc[i + 3][r]} + poison;
+    if (quad == 0)
+        *reinterpret_cast<f32x2_t *>(reinterpret_cast<float *>(area) + (size_t)G * D + 2 * n) =
+            f32x2_t{st.m + poison, l};
+}
+
+// Write a staged partial state to slot `slot` of (part_ml, part_acc) as two
+// contiguous blocks.
+__device__ __forceinline__ void flush_partial(const SplitParams &p, int head_dim, const uint8_t *area, size_t slot,
+                                              int lane)
+{
+    const int G = p.group;
+    const int acc_bytes = G * head_dim * 4;
+    uint8_t *dst = reinterpret_cast<uint8_t *>(p.part_acc + slot * G * head_dim);
+    for (int off = 16 * lane; off < acc_bytes; off += 16 * kWave)
+        *reinterpret_cast<u32x4_t *>(dst + off) = *reinterpret_cast<const u32x4_t *>(area + off);
+    if (lane < G)
+        *reinterpret_cast<f32x2_t *>(p.part_ml + (slot * G + lane) * 2) =
+            *reinterpret_cast<const f32x2_t *>(area + acc_bytes + 8 * lane);
 }
 
 // Turns a[0, n) (in LDS, written before a barrier) into its exclusive
@@ -635,16 +671,21 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
     __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
     uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
-    // Plain attention: per-wave stage of finished units' output rows (see
-    // stage_output), `staged` of them queued, each slot G rows of D bf16.
+    // Plain attention: a per-wave stage (see stage_output) holding the
+    // partial state of the range's first piece, if cut (G * (D + 2) fp32 at
+    // the start), then the output rows of finished units, `staged` of them
+    // queued, each slot G rows of D bf16.
     constexpr bool kStageOut = MODE == kAllPages;
     __shared__ uint8_t out_stage[kWavesPerBlock][kStageOut ? kOutStageBytes : 16];
     __shared__ uint32_t out_rows[kWavesPerBlock][kStageOut ? kMaxOutSlots : 1];
-    uint8_t *const ostage = out_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    uint8_t *const ostage_base = out_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
     uint32_t *const orows = out_rows[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    const int part_bytes = (G * (D + 2) * 4 + 15) & ~15;   // keeps the output slots 16-byte aligned
+    uint8_t *const ostage = ostage_base + part_bytes;
     const int slot_bytes = G * D * 2;
-    const int out_slots = kOutStageBytes / slot_bytes;   // >= 4 (G <= 16, D <= 128)
+    const int out_slots = (kOutStageBytes - part_bytes) / slot_bytes;   // >= 1 (G <= 16, D <= 128)
     int staged = 0;
+    bool part_staged = false;
 
     // Tile entries, fetched in tile order (every call below asks for the next
     // tile; past the range the last tile repeats): {block-table entry (loaded
@@ -821,6 +862,12 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
                             flush_outputs(p, D, ostage, orows, staged, slot_bytes, lane);
                             staged = 0;
                         }
+                    } else if (kStageOut && slot_sel == 0) {
+                        // the range's first piece, cut: written out with the stage at the end
+                        const float l = quad_sum(st.l);
+                        if (n < G)
+                            stage_partial<D>(st, l, bad, ostage_base, G, n, quad);
+                        part_staged = true;
                     } else {
                         finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
                     }
@@ -834,6 +881,8 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     }
     if (kStageOut && staged > 0)
         flush_outputs(p, D, ostage, orows, staged, slot_bytes, lane);
+    if (kStageOut && part_staged)
+        flush_partial(p, D, ostage_base, 2 * (size_t)w, lane);
 }
 
 }  // namespace
