@@ -56,38 +56,54 @@ namespace {
 // count have no pages). Workgroup 0 also stores the sums and every
 // sequence's sharing descriptor for the merge.
 __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const PrefixParams &pp, int32_t *s_own,
-                                                   int32_t *s_len, int32_t *s_group, int32_t *s_sh, int32_t *s_gl)
+                                                   int32_t *s_len, int32_t *s_group, int32_t *s_sh, int32_t *s_gl,
+                                                   int32_t *s_gs, int32_t *s_sp)
 {
     constexpr int T = kWave * kWavesPerBlock;
     const int B = p.batch, NG = pp.num_groups, S = pp.max_sub;
     const int tid = threadIdx.x;
     const int M = prefix_max_members(p.group);
-    const int32_t *gs = pp.group_start;
+    const int32_t *gs = s_gs;   // group_start and shared_pages, read from memory once
     // Scratch for the group passes, in arrays filled only later: s_len (B
     // entries, followed by s_sh, whose first entry takes the scan's total when
     // NG == B) and s_own (B + 1 entries).
     int32_t *const s_prev_end = s_len;   // [NG + 1]: largest end of the earlier groups
     int32_t *const s_base = s_own;       // [NG + 1]: first sub-group of each group
-    // 1. Each group's earlier ends; every sequence starts unmarked.
-    for (int k = tid; k < NG; k += T)
-        s_prev_end[k] = gs[k + 1];
+    // 1. Each group's earlier ends; every sequence starts unmarked. With
+    //    group_start ascending (the usual case) the largest earlier end of
+    //    group k is its own start, and the scan is skipped.
+    bool descends = false;
+    for (int k = tid; k < NG; k += T) {
+        const int lo = pp.group_start[k], hi = pp.group_start[k + 1];
+        s_gs[k] = lo;
+        s_sp[k] = pp.shared_pages[k];
+        if (k == NG - 1)
+            s_gs[NG] = hi;
+        descends |= lo > hi;
+    }
     for (int b = tid; b < B; b += T)
         s_group[b] = -1;
-    __syncthreads();
-    block_exclusive_scan<ScanMax>(s_prev_end, NG);
+    const bool ascending = !__syncthreads_or(descends);
+    if (!ascending) {
+        for (int k = tid; k < NG; k += T)
+            s_prev_end[k] = gs[k + 1];
+        __syncthreads();
+        block_exclusive_scan<ScanMax>(s_prev_end, NG);
+    }
     // 2. Which groups are shared, how many sub-groups each has, and a mark at
     //    each shared group's first member (shared groups never overlap, so no
     //    two marks collide).
     for (int k = tid; k < NG; k += T) {
-        const int lo = gs[k], hi = gs[k + 1], sp = pp.shared_pages[k];
-        const bool ok = lo >= 0 && hi <= B && hi > lo && lo >= s_prev_end[k] && sp > 0 && sp <= p.max_blocks;
+        const int lo = gs[k], hi = gs[k + 1], sp = s_sp[k];
+        const bool ok = lo >= 0 && hi <= B && hi > lo && (ascending || lo >= s_prev_end[k]) && sp > 0 &&
+                        sp <= p.max_blocks;
         s_base[k] = ok ? (hi - lo + M - 1) / M : 0;
         if (ok)
             s_group[lo] = k;
     }
     __syncthreads();
-    block_exclusive_scan<ScanSum>(s_base, NG);
-    block_exclusive_scan<ScanMax>(s_group, B);   // s_group[b + 1]: the latest mark at or before b
+    // s_base: first sub-group of each group; s_group[b + 1]: the latest mark at or before b.
+    block_exclusive_scan2<ScanSum, ScanMax>(s_base, NG, s_group, B);
     // 3. The sub-groups: shared pages and packed first member and size.
     const int NS = s_base[NG];
     for (int sg = tid; sg < S; sg += T) {
@@ -104,7 +120,7 @@ __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const P
             const int lo = gs[klo], m = gs[klo + 1] - lo;
             const int ns = (m + M - 1) / M, cm = (m + ns - 1) / ns;
             const int slo = lo + (sg - s_base[klo]) * cm;
-            sp = pp.shared_pages[klo];
+            sp = s_sp[klo];
             gl = slo | (min(cm, lo + m - slo) - 1) << 16;
         }
         s_sh[sg] = sp;
@@ -148,8 +164,7 @@ __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const P
         s_own[b] = n > sh ? n - sh : 0;
     }
     __syncthreads();
-    block_exclusive_scan<ScanSum>(s_own, B);
-    block_exclusive_scan<ScanSum>(s_sh, S);
+    block_exclusive_scan2<ScanSum, ScanSum>(s_own, B, s_sh, S);
     if (blockIdx.x == 0) {
         for (int i = tid; i <= B; i += T)
             pp.cum_own[i] = s_own[i];
@@ -166,7 +181,7 @@ __device__ __forceinline__ void scan_prefix_groups(const SplitParams &p, const P
 
 // Both passes of prefix-shared attention in one launch (see the top of this
 // file). Every workgroup first derives both streams in its dynamic LDS
-// (prefix_dynamic_lds: 3 B + 2 S + 3 ints, S = pp.max_sub); the number of
+// (prefix_dynamic_lds: 3 B + 2 S + 2 NG + 4 ints, S = pp.max_sub); the number of
 // shared-page workers that take part is effective_shared_workers of the
 // own-page total, as in the merge.
 template <int D, bool FP8>
@@ -181,7 +196,9 @@ __global__ __launch_bounds__(kWave * kWavesPerBlock) void prefix_split_kernel(Sp
     int32_t *const s_len = s_group + B + 1;   // [B]
     int32_t *const s_sh = s_len + B;          // [S + 1]
     int32_t *const s_gl = s_sh + S + 1;       // [S]
-    scan_prefix_groups(own, pp, s_own, s_len, s_group, s_sh, s_gl);
+    int32_t *const s_gs = s_gl + S;           // [NG + 1]
+    int32_t *const s_sp = s_gs + pp.num_groups + 1;   // [NG]
+    scan_prefix_groups(own, pp, s_own, s_len, s_group, s_sh, s_gl, s_gs, s_sp);
     if ((int)blockIdx.x < own_blocks)
         split_unit_worker<D, FP8, kOwnPages>(
             own, blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
@@ -204,7 +221,7 @@ hipError_t launch_prefix_split(const SplitParams &own, const SplitParams &shared
     const int own_blocks = (own.num_workers + kWavesPerBlock - 1) / kWavesPerBlock;
     const dim3 grid(own_blocks + max_shared);
     const dim3 block(kWave * kWavesPerBlock);
-    const size_t lds = prefix_dynamic_lds(own.batch, pp.max_sub);
+    const size_t lds = prefix_dynamic_lds(own.batch, pp.max_sub, pp.num_groups);
 #define SL_PREFIX(DD, FF) \
     hipLaunchKernelGGL((prefix_split_kernel<DD, FF>), grid, block, lds, stream, own, shared, pp, own_blocks, max_shared)
     if (head_dim == 128 && !fp8)

@@ -596,6 +596,68 @@ __device__ __forceinline__ void block_exclusive_scan(int32_t *a, int n)
     __syncthreads();
 }
 
+// Two independent exclusive scans, a[0, n) under OpA and b[0, m) under OpB,
+// with their totals in a[n] and b[m], sharing the barriers of one scan.
+template <class OpA, class OpB>
+__device__ __forceinline__ void block_exclusive_scan2(int32_t *a, int n, int32_t *b, int m)
+{
+    __shared__ int32_t s_wave[2][kWavesPerBlock];
+    constexpr int T = kWave * kWavesPerBlock;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int pa = (n + T - 1) / T, pb = (m + T - 1) / T;
+    const int alo = min(n, tid * pa), ahi = min(n, alo + pa);
+    const int blo = min(m, tid * pb), bhi = min(m, blo + pb);
+    int la = OpA::kIdentity, lb = OpB::kIdentity;
+    for (int i = alo; i < ahi; ++i)
+        la = OpA::op(la, a[i]);
+    for (int i = blo; i < bhi; ++i)
+        lb = OpB::op(lb, b[i]);
+    int ia = la, ib = lb;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int va = __shfl_up(ia, off, kWave);
+        const int vb = __shfl_up(ib, off, kWave);
+        if (lane >= off) {
+            ia = OpA::op(ia, va);
+            ib = OpB::op(ib, vb);
+        }
+    }
+    const int ea = __shfl_up(ia, 1, kWave), eb = __shfl_up(ib, 1, kWave);
+    if (lane == kWave - 1) {
+        s_wave[0][wave] = ia;
+        s_wave[1][wave] = ib;
+    }
+    __syncthreads();
+    int base_a = OpA::kIdentity, tot_a = OpA::kIdentity, base_b = OpB::kIdentity, tot_b = OpB::kIdentity;
+#pragma unroll
+    for (int k = 0; k < kWavesPerBlock; ++k) {
+        if (k < wave) {
+            base_a = OpA::op(base_a, s_wave[0][k]);
+            base_b = OpB::op(base_b, s_wave[1][k]);
+        }
+        tot_a = OpA::op(tot_a, s_wave[0][k]);
+        tot_b = OpB::op(tot_b, s_wave[1][k]);
+    }
+    int ra = OpA::op(base_a, lane > 0 ? ea : OpA::kIdentity);
+    for (int i = alo; i < ahi; ++i) {
+        const int v = a[i];
+        a[i] = ra;
+        ra = OpA::op(ra, v);
+    }
+    int rb = OpB::op(base_b, lane > 0 ? eb : OpB::kIdentity);
+    for (int i = blo; i < bhi; ++i) {
+        const int v = b[i];
+        b[i] = rb;
+        rb = OpB::op(rb, v);
+    }
+    if (tid == 0) {
+        a[n] = tot_a;
+        b[m] = tot_b;
+    }
+    __syncthreads();
+}
+
 // Pages of a sequence of length L: ceil(clamp(L, 0, max_len) / 16).
 __device__ __forceinline__ int pages_of(int L, int max_len)
 {
@@ -621,6 +683,17 @@ __device__ __forceinline__ void scan_sequences(const SplitParams &p, int32_t *s_
     if (blockIdx.x == 0)
         for (int b = threadIdx.x; b <= B; b += T)
             p.cum_out[b] = s_cum[b];
+}
+
+// This wave's staging area for regrouping K tiles (16 tokens x D elements).
+// Declared here, keyed only on the tile shape, so that a kernel running the
+// worker in several modes (prefix sharing: own and shared pages in different
+// workgroups) holds one such array, not one per mode.
+template <int D, bool FP8>
+__device__ __forceinline__ uint8_t *k_regroup_stage()
+{
+    __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
+    return k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
 }
 
 // Which tiles a worker streams.
@@ -668,9 +741,7 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     const int n = lane & 15;
     const int quad = lane >> 4;
     const int G = p.group;
-    // Per-wave staging area for regrouping K tiles (16 tokens x D elements).
-    __shared__ uint8_t k_stage[kWavesPerBlock][kPageSize * D * (FP8 ? 1 : 2)];
-    uint8_t *lds = k_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    uint8_t *lds = k_regroup_stage<D, FP8>();
     // Plain attention: a per-wave stage (see stage_output) holding the
     // partial state of the range's first piece, if cut (G * (D + 2) fp32 at
     // the start), then the output rows of finished units, `staged` of them

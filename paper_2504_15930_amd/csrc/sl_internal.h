@@ -237,10 +237,11 @@ size_t workspace_layout(void *base, int batch, int max_blocks, int num_kv_heads,
 inline size_t split_dynamic_lds(int batch) { return sizeof(int32_t) * (2 * (size_t)batch + 1); }
 // The fused prefix kernel's: for the sequences the own-page prefix sum, the
 // sub-groups and the lengths (3 B + 2 ints), for the sub-groups the
-// shared-page prefix sum and the packed first member and size (2 S + 1 ints).
-inline size_t prefix_dynamic_lds(int batch, int max_sub)
+// shared-page prefix sum and the packed first member and size (2 S + 1 ints),
+// and the groups' starts and page counts (2 NG + 1 ints).
+inline size_t prefix_dynamic_lds(int batch, int max_sub, int num_groups)
 {
-    return sizeof(int32_t) * (3 * (size_t)batch + 2 * (size_t)max_sub + 3);
+    return sizeof(int32_t) * (3 * (size_t)batch + 2 * (size_t)max_sub + 2 * (size_t)num_groups + 4);
 }
 hipError_t launch_split(const SplitParams &p, int head_dim, bool fp8, hipStream_t stream);
 // Prefix mode: the own-page pass (single-unit workers) and the shared-page
