@@ -16,6 +16,15 @@
 // saves a copy command per step; a ring of such buffers, each reused only
 // once the kernels that read it have completed, lets the host run ahead of
 // the GPU.
+//
+// A bf16 step whose attention fits the chip in one pass of workgroups runs
+// in a single launch instead (engine_unit_step_kernel): the host passes the
+// step's sequences and lengths as kernel arguments, gives each (sequence, KV
+// head) unit a share of the CUs in whole workgroups, and the unit's
+// workgroups combine their states themselves; the next step's append rides
+// in the same launch unless it would reuse a page freed in this step, which
+// this step's attention may still be reading. Empty slots' rows are cleared
+// once per run call and whenever a slot empties.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -24,12 +33,18 @@
 #include "sl.h"
 #include "sl_engine.h"
 #include "api_internal.h"
-#include "sl_internal.h"
+#include "engine_internal.h"
 
 namespace {
 
 using sl::kPageSize;
 constexpr int kRing = 8;
+// One-launch step: a wave gets at least this many tiles of its unit, and the
+// step takes the one-launch path only while its longest wave range is within
+// kUnitSlackTiles tiles of a split-kernel worker's share (the two-launch
+// step spreads tiles over all workers but pays a second launch).
+constexpr int kUnitMinTiles = 1;
+constexpr int kUnitSlackTiles = 8;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -59,6 +74,15 @@ struct sl_engine {
     bool ev_pending[kRing] = {};
     int ring = 0;
 
+    // One-launch step (bf16): device memory for the pieces and the arrival
+    // counters, the CU and split-worker counts, which slots' rows are known
+    // to be zero, and whether a sample finished in the current step.
+    void *unit_mem = nullptr;
+    int cus = 0, nw = 0;
+    sl::UnitStepParams up{};
+    std::vector<uint8_t> zeroed;
+    bool freed_now = false;
+
     void release()
     {
         for (int r = 0; r < kRing; ++r) {
@@ -67,6 +91,8 @@ struct sl_engine {
             if (h_stage[r])
                 (void)hipHostFree(h_stage[r]);
         }
+        if (unit_mem)
+            (void)hipFree(unit_mem);
     }
 
     // A step's staging: ring slot, update and fill counts, active samples.
@@ -81,6 +107,7 @@ struct sl_engine {
     sl_status prepare(Staged &out);
     sl::AppendParams append_params(const Staged &sg) const;
     sl_status launch_staged(const Staged &sg);
+    bool plan_unit_step(const Staged &sg);
     sl_status one_step(bool chain);
 };
 
@@ -185,6 +212,53 @@ sl_status sl_engine::launch_staged(const Staged &sg)
     return SL_OK;
 }
 
+// Fill `up` for a one-launch step over the lengths staged in `sg`, or
+// return false if the step should take the two-launch path.
+bool sl_engine::plan_unit_step(const Staged &sg)
+{
+    if (!unit_mem)
+        return false;
+    const int32_t *h = h_stage[sg.ring];
+    int n = 0, z = 0;
+    long long tiles = 0;   // per KV head
+    for (int b = 0; b < BS; ++b) {
+        if (h[b] > 0) {
+            if (n == sl::kMaxUnitEntries)
+                return false;
+            up.seq[n] = b;
+            up.len[n] = h[b];
+            ++n;
+            tiles += (h[b] + kPageSize - 1) / kPageSize;
+        } else if (!zeroed[b]) {
+            if (z == sl::kMaxUnitEntries)
+                return false;
+            up.zero[z++] = b;
+        }
+    }
+    if (n == 0 || (long long)n * Hkv > cus)
+        return false;
+    // Workgroups per unit: its share of the CUs by tiles, at least one, and
+    // at most enough to give every wave kUnitMinTiles tiles.
+    int blocks = 0, wave_tiles = 0;
+    for (int e = 0; e < n; ++e) {
+        const int nb = (up.len[e] + kPageSize - 1) / kPageSize;
+        long long k = (long long)cus * nb / (tiles * Hkv);
+        const long long kmax = (nb + sl::kUnitWaves * kUnitMinTiles - 1) / (sl::kUnitWaves * kUnitMinTiles);
+        k = std::max(1LL, std::min(std::min(k, kmax), (long long)sl::kMaxUnitSplit));
+        up.first[e] = blocks;
+        blocks += Hkv * (int)k;
+        wave_tiles = std::max(wave_tiles, (int)((nb + sl::kUnitWaves * k - 1) / (sl::kUnitWaves * k)));
+    }
+    up.first[n] = blocks;
+    const long long worker_tiles = (tiles * Hkv + nw - 1) / nw;
+    if (blocks > sl::kMaxUnitBlocks || wave_tiles > worker_tiles + kUnitSlackTiles)
+        return false;
+    up.n_entries = n;
+    up.unit_blocks = blocks;
+    up.zero_blocks = z;
+    return true;
+}
+
 sl_status sl_engine::one_step(bool chain)
 {
     // This step's bookkeeping and KV append: launched now, unless the previous
@@ -207,14 +281,17 @@ sl_status sl_engine::one_step(bool chain)
     }
     next_state = kNone;
 
+    const int this_step = step;
     // The step's tokens are decided: every occupied slot makes one; finished
     // samples leave and give their pages back, last block first.
     active.push_back(cur.n_active);
+    freed_now = false;
     for (int b = 0; b < BS; ++b) {
         const int i = occupant[b];
         if (i < 0)
             continue;
         if (++made[b] == outlen[i]) {
+            freed_now = true;
             finish[i] = step;
             for (auto it = pages[b].rbegin(); it != pages[b].rend(); ++it)
                 free_stack.push_back(*it);
@@ -225,34 +302,62 @@ sl_status sl_engine::one_step(bool chain)
     ++step;
 
     // With more steps to run, stage the next one now. Its bookkeeping and KV
-    // append then run in this step's merge launch, after the attention has
-    // read the cache, unless it admits prompts: their pages must be filled
-    // before the append, so that step launches them itself.
+    // append then run in this step's last launch, after (or, in the
+    // one-launch step, beside) the attention, unless it admits prompts: their
+    // pages must be filled before the append, so that step launches them
+    // itself. Beside the attention it also must not reuse a page freed in
+    // this step: the free stack hands those out first.
     const sl::AppendParams *fused = nullptr;
     sl::AppendParams nap;
-    bool last = false;
+    bool last = false, fuse = false;
     if (chain) {
         st = prepare(next);
         if (st != SL_OK)
             return st;
-        if (next.n_active == 0) {
+        if (next.n_active == 0)
             last = true;
-        } else if (next.n_fill == 0) {
+        else
+            fuse = next.n_fill == 0;
+    }
+    const bool one_launch = plan_unit_step(cur);
+    if (one_launch && freed_now && next.n_upd > 0)
+        fuse = false;
+    if (chain && !last) {
+        next_state = fuse ? kLaunched : kPrepared;
+        if (fuse) {
             nap = append_params(next);
             fused = &nap;
-            next_state = kLaunched;
-        } else {
-            next_state = kPrepared;
         }
     }
-    if (fp8)
-        st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, buf.k_scales, buf.v_scales,
-                                         buf.block_table, buf.seq_lens, attn_scale, buf.out, true, fused);
-    else
-        st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, nullptr, nullptr,
-                                         buf.block_table, buf.seq_lens, attn_scale, buf.out, false, fused);
-    if (st != SL_OK)
-        return st;
+    if (one_launch) {
+        up.next = fused ? *fused : sl::AppendParams{};
+        up.next_blocks = fused ? (BS * Hkv + sl::kUnitWaves - 1) / sl::kUnitWaves : 0;
+        if (sl::launch_unit_step(up, D, step_desc.stream) != hipSuccess)
+            return SL_ERR_HIP;
+        for (int e = 0; e < up.n_entries; ++e)
+            zeroed[up.seq[e]] = 0;
+        for (int z = 0; z < up.zero_blocks; ++z)
+            zeroed[up.zero[z]] = 1;
+    } else {
+        if (fp8)
+            st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, buf.k_scales,
+                                             buf.v_scales, buf.block_table, buf.seq_lens, attn_scale, buf.out, true,
+                                             fused);
+        else
+            st = sl::decode_attn_then_append(&step_desc, buf.q, buf.k_pages, buf.v_pages, nullptr, nullptr,
+                                             buf.block_table, buf.seq_lens, attn_scale, buf.out, false, fused);
+        if (st != SL_OK)
+            return st;
+        const int32_t *h = h_stage[cur.ring];   // the merge writes every empty slot's rows
+        for (int b = 0; b < BS; ++b)
+            zeroed[b] = h[b] <= 0;
+    }
+    if (buf.out_history && this_step < buf.history_steps) {
+        const size_t bytes = sizeof(uint16_t) * BS * step_desc.num_q_heads * D;
+        if (hipMemcpyAsync(buf.out_history + (size_t)this_step * (bytes / sizeof(uint16_t)), buf.out, bytes,
+                           hipMemcpyDeviceToDevice, step_desc.stream) != hipSuccess)
+            return SL_ERR_HIP;
+    }
     if (fused) {
         if (hipEventRecord(ev[next.ring], step_desc.stream) != hipSuccess)
             return SL_ERR_HIP;
@@ -278,8 +383,11 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     if (!d.workspace || d.workspace_bytes < need || !aligned(d.workspace, 256))
         return SL_ERR_WORKSPACE;
     const int M = cfg->num_samples, BS = d.batch;
-    if (M < 1 || BS < 1 || (cfg->admission != 0 && cfg->admission != 1))
+    if (M < 1 || BS < 1 || (cfg->admission != 0 && cfg->admission != 1) ||
+        (cfg->launch_mode != 0 && cfg->launch_mode != 1) || bufs->history_steps < 0)
         return SL_ERR_SHAPE;
+    if (bufs->history_steps > 0 && !bufs->out_history)
+        return SL_ERR_NULL;
     if (!cfg->prompt_len || !cfg->output_len || !cfg->est_len)
         return SL_ERR_NULL;
     if (!bufs->q || !bufs->k_new || !bufs->v_new || !bufs->k_pages || !bufs->v_pages || !bufs->block_table ||
@@ -290,7 +398,7 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
         return SL_ERR_NULL;
     if (!aligned(bufs->q, 16) || !aligned(bufs->out, 16) || !aligned(bufs->k_pages, 16) ||
         !aligned(bufs->v_pages, 16) || !aligned(bufs->k_new, 4) || !aligned(bufs->v_new, 4) ||
-        !aligned(bufs->block_table, 4) || !aligned(bufs->seq_lens, 4) ||
+        !aligned(bufs->block_table, 4) || !aligned(bufs->seq_lens, 4) || !aligned(bufs->out_history, 16) ||
         (fp8 && (!aligned(bufs->k_scales, 4) || !aligned(bufs->v_scales, 4))))
         return SL_ERR_ALIGNMENT;
     int max_prompt_blocks = 0;
@@ -339,6 +447,63 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     e->finish.assign(M, -1);
     // staging: lengths, token pages, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
     e->stage_ints = 2 * (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
+    e->zeroed.assign(BS, 0);
+    // One-launch step (bf16): piece slots (kMaxUnitBlocks workgroups, each G
+    // pairs (m, l) on whole cache lines and G rows of D accumulators) and the
+    // arrival counters, zeroed.
+    if (!fp8 && cfg->launch_mode == 0) {
+        const int G = d.num_q_heads / d.num_kv_heads;
+        int dev = 0, nw = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&e->cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+            delete e;
+            return SL_ERR_HIP;
+        }
+        st = sl_decode_attn_num_workers(&d, 0, &nw);
+        if (st != SL_OK) {
+            delete e;
+            return st;
+        }
+        e->nw = nw;
+        const size_t rows = (size_t)sl::kMaxUnitBlocks * G;
+        const size_t ml_bytes = (size_t)sl::kMaxUnitBlocks * sl::unit_ml_stride(G) * sizeof(float);
+        const size_t acc_bytes = (rows * d.head_dim * sizeof(float) + 255) / 256 * 256;
+        const size_t cnt_bytes = sizeof(int32_t) * sl::kMaxUnitEntries * d.num_kv_heads;
+        if (hipMalloc(&e->unit_mem, ml_bytes + acc_bytes + cnt_bytes) != hipSuccess) {
+            e->unit_mem = nullptr;
+            delete e;
+            return SL_ERR_HIP;
+        }
+        char *base = static_cast<char *>(e->unit_mem);
+        if (hipMemset(base + ml_bytes + acc_bytes, 0, cnt_bytes) != hipSuccess) {
+            e->release();
+            delete e;
+            return SL_ERR_HIP;
+        }
+        sl::SplitParams &sp = e->up.cur;
+        sp.q = bufs->q;
+        sp.k_pages = bufs->k_pages;
+        sp.v_pages = bufs->v_pages;
+        sp.k_scales = nullptr;
+        sp.v_scales = nullptr;
+        sp.out = bufs->out;
+        sp.part_ml = reinterpret_cast<float *>(base);
+        sp.part_acc = reinterpret_cast<float *>(base + ml_bytes);
+        sp.batch = BS;
+        sp.num_kv_heads = d.num_kv_heads;
+        sp.group = G;
+        sp.num_workers = 0;
+        sp.num_q_heads = d.num_q_heads;
+        sp.scale_log2 = cfg->attn_scale * 1.4426950408889634f;
+        sp.unit_ml = nullptr;
+        sp.unit_acc = nullptr;
+        sp.seq_lens = nullptr;
+        sp.block_table = bufs->block_table;
+        sp.cum_out = nullptr;
+        sp.max_blocks = d.max_blocks_per_seq;
+        sp.num_pages = d.num_pages;
+        e->up.counters = reinterpret_cast<int32_t *>(base + ml_bytes + acc_bytes);
+    }
     bool ok = true;
     for (int r = 0; ok && r < kRing; ++r)
         ok = hipHostMalloc(reinterpret_cast<void **>(&e->h_stage[r]), sizeof(int32_t) * e->stage_ints,
@@ -363,6 +528,8 @@ sl_status sl_engine_run(sl_engine *e, int32_t max_steps, int32_t *steps_run)
     *steps_run = 0;
     if (e->failed != SL_OK)
         return e->failed;
+    // The caller may have written `out` between calls: clear empty slots' rows again.
+    std::fill(e->zeroed.begin(), e->zeroed.end(), 0);
     for (int k = 0; k < max_steps && !e->done; ++k) {
         const int before = e->step;
         const sl_status st = e->one_step(k + 1 < max_steps);

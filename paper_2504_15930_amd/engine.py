@@ -25,6 +25,7 @@ class Config(ctypes.Structure):
         ("prompt_len", ctypes.c_void_p),
         ("output_len", ctypes.c_void_p),
         ("est_len", ctypes.c_void_p),
+        ("launch_mode", ctypes.c_int32),
     ]
 
 
@@ -41,6 +42,8 @@ class Buffers(ctypes.Structure):
         ("block_table", ctypes.c_void_p),
         ("seq_lens", ctypes.c_void_p),
         ("out", ctypes.c_void_p),
+        ("out_history", ctypes.c_void_p),
+        ("history_steps", ctypes.c_int32),
     ]
 
 
@@ -63,13 +66,15 @@ class Engine:
 
     Allocates (with torch) the page pool, block table, lengths, query and
     new-row buffers, output and workspace; ``q``/``k_new``/``v_new`` hold
-    seeded random rows used in every step.
+    seeded random rows used in every step. ``two_launch`` makes every bf16
+    step run the split kernel and the merge; ``history_steps`` > 0 keeps the
+    outputs of the first that many steps in ``history``.
     """
 
     def __init__(self, prompt_len, output_len, est_len=None, *, batch_slots: int, num_q_heads: int,
                  num_kv_heads: int, head_dim: int, kv_fp8: bool = False, lpt: bool = True,
                  num_pages: int | None = None, max_blocks: int | None = None, seed: int = 0,
-                 num_workers: int = 0, device="cuda:0"):
+                 num_workers: int = 0, two_launch: bool = False, history_steps: int = 0, device="cuda:0"):
         self.prompt_len = np.ascontiguousarray(prompt_len, dtype=np.int32)
         self.output_len = np.ascontiguousarray(output_len, dtype=np.int32)
         self.est_len = np.ascontiguousarray(self.output_len if est_len is None else est_len, dtype=np.int32)
@@ -93,6 +98,8 @@ class Engine:
         self.k_new = torch.randn((batch_slots, num_kv_heads, head_dim), generator=g, device=dev).to(torch.bfloat16)
         self.v_new = torch.randn((batch_slots, num_kv_heads, head_dim), generator=g, device=dev).to(torch.bfloat16)
         self.out = torch.zeros((batch_slots, num_q_heads, head_dim), dtype=torch.bfloat16, device=dev)
+        self.history = (torch.zeros((history_steps, batch_slots, num_q_heads, head_dim), dtype=torch.bfloat16,
+                                    device=dev) if history_steps > 0 else None)
         self.scale = float(np.float32(1.0 / np.sqrt(head_dim)))
         self.stream = torch.cuda.current_stream(dev)
         desc = sl.make_desc(batch_slots, num_q_heads, num_kv_heads, head_dim, 16, self.max_blocks,
@@ -103,9 +110,10 @@ class Engine:
         ptr = lambda t: None if t is None else t.data_ptr()
         self._bufs = Buffers(desc, ptr(self.q), ptr(self.k_new), ptr(self.v_new), ptr(self.k_pages),
                              ptr(self.v_pages), ptr(self.k_scales), ptr(self.v_scales), ptr(self.block_table),
-                             ptr(self.seq_lens), ptr(self.out))
+                             ptr(self.seq_lens), ptr(self.out), ptr(self.history), int(history_steps))
         self._cfg = Config(M, 1 if lpt else 0, 1 if kv_fp8 else 0, seed & 0xFFFFFFFF, self.scale,
-                           self.prompt_len.ctypes.data, self.output_len.ctypes.data, self.est_len.ctypes.data)
+                           self.prompt_len.ctypes.data, self.output_len.ctypes.data, self.est_len.ctypes.data,
+                           1 if two_launch else 0)
         torch.cuda.synchronize(dev)
         handle = ctypes.c_void_p()
         sl._check(_lib().sl_engine_create(ctypes.byref(self._cfg), ctypes.byref(self._bufs), ctypes.byref(handle)),

@@ -172,6 +172,15 @@ def test_engine_rejects_bad_arguments(lib):
     assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(bufs), ctypes.byref(handle)) == -4  # no workspace
     bad = E.Buffers(_desc(batch=2, head_dim=96), *([FAKE] * 10))
     assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(bad), ctypes.byref(handle)) == -3
+    # with a (never touched) workspace: the launch mode, the output history and its alignment
+    d = _desc(batch=2, max_blocks=4, num_pages=8)
+    d.workspace, d.workspace_bytes = FAKE, 1 << 30
+    mode = E.Config(2, 1, 0, 0, 0.125, ctypes.addressof(lens), ctypes.addressof(outs), ctypes.addressof(outs), 2)
+    assert lib.sl_engine_create(ctypes.byref(mode), ctypes.byref(E.Buffers(d, *([FAKE] * 10))),
+                                ctypes.byref(handle)) == -2
+    for hist, steps, status in [(None, 3, -1), (FAKE, -1, -2), (FAKE + 8, 1, -6)]:
+        b = E.Buffers(d, *([FAKE] * 10), hist, steps)
+        assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(b), ctypes.byref(handle)) == status
     n = ctypes.c_int32(0)
     assert lib.sl_engine_run(None, 1, ctypes.byref(n)) == -1
     assert lib.sl_engine_destroy(None) == 0

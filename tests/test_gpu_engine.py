@@ -31,13 +31,14 @@ def _case(seed, M, lo_p=0, hi_p=100, med_o=40):
     return prompt, out, est
 
 
-@pytest.mark.parametrize("fp8", [False, True], ids=["bf16", "e4m3"])
+@pytest.mark.parametrize("mode", ["bf16", "bf16-two-launch", "e4m3"])
 @pytest.mark.parametrize("lpt", [True, False], ids=["lpt", "fifo"])
-def test_engine_matches_oracle(lpt, fp8):
+def test_engine_matches_oracle(lpt, mode):
+    fp8 = mode == "e4m3"
     prompt, out, est = _case(11 if lpt else 12, M=30)
     BS, Hq, Hkv, D = 6, 8, 2, 128
     eng = E.Engine(prompt, out, est, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D,
-                   kv_fp8=fp8, lpt=lpt, seed=3)
+                   kv_fp8=fp8, lpt=lpt, seed=3, two_launch=mode == "bf16-two-launch")
     ref = S.simulate(prompt, out, est, BS, eng.num_pages, eng.max_blocks, "lpt" if lpt else "fifo",
                      checkpoints=range(0, 10000))
     checks = [0, 1, 2, 7, 16, 33, ref.makespan // 2, ref.makespan - 1]
@@ -96,3 +97,78 @@ def test_engine_lpt_beats_fifo_on_long_tail():
         assert spans[lpt] == ref.makespan
         eng.close()
     assert spans[True] < spans[False]
+
+
+def test_engine_one_launch_long_contexts():
+    """bf16 cache, 32 slots of 7B-like heads with prompts of 300-1500 tokens: the one-launch step
+    gives every unit several workgroups, whose pieces the last one to arrive merges. Checked at
+    checkpoints against the oracle, after runs of one and of many steps."""
+    rng = np.random.default_rng(21)
+    M, BS, Hq, Hkv, D = 48, 32, 28, 4, 128
+    prompt = rng.integers(300, 1500, M).astype(np.int32)
+    out = np.clip(np.exp(rng.normal(np.log(60), 0.8, M)), 1, 200).astype(np.int32)
+    eng = E.Engine(prompt, out, out, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True,
+                   seed=4)
+    ref = S.simulate(prompt, out, out, BS, eng.num_pages, eng.max_blocks, "lpt", checkpoints=range(0, 10000))
+    done = 0
+    for c in [0, 1, 2, 3, 9, 10, 40, ref.makespan // 2, ref.makespan - 2, ref.makespan - 1]:
+        print("one-launch engine checkpoint", c, flush=True)
+        done += eng.run(c + 1 - done)
+        assert done == c + 1
+        torch.cuda.synchronize()
+        lens = eng.seq_lens.cpu().numpy()
+        table = eng.block_table.cpu().numpy()
+        want_lens, want_table = ref.checkpoints[c]
+        assert lens.tolist() == want_lens, f"step {c}: lengths"
+        want = oracle.decode_attn(_host_u16(eng.q), _host_u16(eng.k_pages), _host_u16(eng.v_pages), table, lens,
+                                  eng.scale)
+        parity.assert_parity(eng.out, want, f"one-launch attention at step {c}")
+    eng.close()
+
+
+@pytest.mark.parametrize("queries", ["zero", "random"])
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 128), (16, 1, 64)], ids=["G4-D128", "G16-D64"])
+def test_engine_one_launch_every_step_matches_two_launch(Hq, Hkv, D, queries):
+    """Every step's output of a whole generation, kept in the engine's output history, with one
+    launch per step against split + merge (whose steps the oracle checks above). The samples finish
+    often, open pages often (prompts of 0, 16, 32 tokens among them) and include one 3000-token
+    prompt, so the steps cover units of one and of many workgroups, empty slots, admissions beside
+    finishes, and next-step appends that take a page freed in the same step (those run in a launch
+    of their own).
+
+    Zero queries make every weight exactly 1: both paths then compute the mean of the value rows
+    and may differ only in the last place of the bf16 output, while a row read at the wrong time
+    would move the mean by its change over the length. With random queries each path rounds its
+    weights to bf16 against its own running maxima, an error of at most 2^-9 of the spread of the
+    value rows around the output each (bounded by 2 max |v|), so the paths may differ by
+    2^-7 max |v| plus two units in the last place."""
+    rng = np.random.default_rng(33)
+    M, BS = 60, 16
+    prompt = rng.choice(np.array([0, 16, 32, 5, 47, 100, 260], np.int32), M)
+    prompt[7] = 3000
+    out = np.clip(np.exp(rng.normal(np.log(12), 0.9, M)), 1, 60).astype(np.int32)
+    ref = S.simulate(prompt, out, out, BS, BS * int(((prompt + out + 15) // 16).max()),
+                     int(((prompt + out + 15) // 16).max()), "lpt")
+    steps = ref.makespan
+    hist = {}
+    vmax = 2.0   # synthetic prompt values are uniform in [-2, 2)
+    for two in (False, True):
+        eng = E.Engine(prompt, out, out, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True,
+                       seed=9, two_launch=two, history_steps=steps)
+        if queries == "zero":
+            eng.q.zero_()
+        vmax = max(vmax, float(eng.v_new.float().abs().max()))
+        assert eng.run() == steps
+        torch.cuda.synchronize()
+        hist[two] = eng.history.float().cpu()
+        eng.close()
+    a, b = hist[False], hist[True]
+    assert torch.isfinite(a).all() and torch.isfinite(b).all()
+    mag = torch.maximum(a.abs(), b.abs()).clamp_min(2.0 ** -126)
+    ulp = torch.exp2(torch.floor(torch.log2(mag)) - 7)   # bf16 spacing at the larger magnitude
+    bound = ulp + 1e-5 if queries == "zero" else 2 * ulp + 2.0 ** -7 * vmax
+    err = (a - b).abs()
+    bad = err > bound
+    assert not bad.any(), (f"{int(bad.sum())} elements differ, first at step "
+                           f"{int(bad.nonzero()[0, 0])}, max |diff| {float(err.max()):.3g}")
+    print(f"one-launch vs two-launch: max |diff| {float(err.max()):.3g} over {steps} steps", flush=True)
