@@ -551,6 +551,37 @@ __device__ __forceinline__ void flush_partial(const SplitParams &p, int head_dim
             *reinterpret_cast<const f32x2_t *>(area + acc_bytes + 8 * lane);
 }
 
+// Prefix own pages: the fp32 states of finished own units that the merge
+// combines are queued per wave in LDS and written when the queue is full or
+// the range ends, for the reason given above for the output stage. The queue
+// holds two states at G <= 8 (D = 128) and stays small, so the fused prefix
+// kernel keeps two workgroups per CU (a 16 KB queue per wave did not).
+constexpr int kOwnStageBytes = 8448;                        // per wave
+constexpr int kMaxOwnSlots = kOwnStageBytes / ((1 * (64 + 2) * 4 + 15) & ~15);
+
+// Write `count` queued states: entry s holds G rows of D fp32 (acc) and G
+// pairs (m, l) as stage_partial lays them out; dest[s] = slot << 1 | (unit
+// area ? 1 : 0), the slot in (part_ml, part_acc) or (unit_ml, unit_acc).
+__device__ __forceinline__ void flush_states(const SplitParams &p, int head_dim, const uint8_t *stage,
+                                             const uint32_t *dest, int count, int area_bytes, int lane)
+{
+    const int G = p.group;
+    const int acc_bytes = G * head_dim * 4;
+    for (int s = 0; s < count; ++s) {
+        const uint32_t d = dest[s];
+        const size_t slot = d >> 1;
+        float *const pml = (d & 1u) ? p.unit_ml : p.part_ml;
+        float *const pacc = (d & 1u) ? p.unit_acc : p.part_acc;
+        const uint8_t *area = stage + (size_t)s * area_bytes;
+        uint8_t *dst = reinterpret_cast<uint8_t *>(pacc + slot * G * head_dim);
+        for (int off = 16 * lane; off < acc_bytes; off += 16 * kWave)
+            *reinterpret_cast<u32x4_t *>(dst + off) = *reinterpret_cast<const u32x4_t *>(area + off);
+        if (lane < G)
+            *reinterpret_cast<f32x2_t *>(pml + (slot * G + lane) * 2) =
+                *reinterpret_cast<const f32x2_t *>(area + acc_bytes + 8 * lane);
+    }
+}
+
 // Turns a[0, n) (in LDS, written before a barrier) into its exclusive
 // prefix scan under Op (sum or maximum) and stores the total in a[n]. Every
 // thread of the workgroup calls it; each scans a contiguous run. Ends with a
@@ -757,6 +788,14 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
     const int out_slots = (kOutStageBytes - part_bytes) / slot_bytes;   // >= 1 (G <= 16, D <= 128)
     int staged = 0;
     bool part_staged = false;
+    // Prefix own pages: the queue of finished own units' states (flush_states).
+    constexpr bool kStageOwn = MODE == kOwnPages;
+    __shared__ uint8_t own_stage[kWavesPerBlock][kStageOwn ? kOwnStageBytes : 16];
+    __shared__ uint32_t own_dest[kWavesPerBlock][kStageOwn ? kMaxOwnSlots : 1];
+    uint8_t *const qstage = own_stage[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    uint32_t *const qdest = own_dest[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];
+    const int own_slots = kStageOwn ? kOwnStageBytes / part_bytes : 0;   // 1 or more (G <= 16, D <= 128)
+    int queued = 0;
 
     // Tile entries, fetched in tile order (every call below asks for the next
     // tile; past the range the last tile repeats): {block-table entry (loaded
@@ -939,6 +978,18 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
                         if (n < G)
                             stage_partial<D>(st, l, bad, ostage_base, G, n, quad);
                         part_staged = true;
+                    } else if (kStageOwn && !(whole && !to_unit)) {
+                        // a state the merge combines: queued
+                        const float l = quad_sum(st.l);
+                        if (queued == own_slots) {
+                            flush_states(p, D, qstage, qdest, queued, part_bytes, lane);
+                            queued = 0;
+                        }
+                        if (n < G)
+                            stage_partial<D>(st, l, bad, qstage + (size_t)queued * part_bytes, G, n, quad);
+                        if (lane == 0)
+                            qdest[queued] = (uint32_t)(slot << 1) | (to_unit ? 1u : 0u);
+                        ++queued;
                     } else {
                         finish_unit<D>(p, st, row0, whole && !to_unit, bad, pml, pacc, slot, n, quad);
                     }
@@ -954,6 +1005,8 @@ __device__ __forceinline__ void split_unit_worker(const SplitParams &p, int w, c
         flush_outputs(p, D, ostage, orows, staged, slot_bytes, lane);
     if (kStageOut && part_staged)
         flush_partial(p, D, ostage_base, 2 * (size_t)w, lane);
+    if (kStageOwn && queued > 0)
+        flush_states(p, D, qstage, qdest, queued, part_bytes, lane);
 }
 
 }  // namespace
