@@ -172,3 +172,31 @@ def test_engine_one_launch_every_step_matches_two_launch(Hq, Hkv, D, queries):
     assert not bad.any(), (f"{int(bad.sum())} elements differ, first at step "
                            f"{int(bad.nonzero()[0, 0])}, max |diff| {float(err.max()):.3g}")
     print(f"one-launch vs two-launch: max |diff| {float(err.max()):.3g} over {steps} steps", flush=True)
+
+
+def test_engine_clears_empty_rows_after_caller_writes_out():
+    """The one-launch step clears an empty slot's output rows once, not every step. A caller that
+    writes `out` between run calls (here: NaN everywhere) must still find zero rows for the empty
+    slots, and the oracle's rows for the others, after the next call."""
+    prompt = np.array([40, 7, 300, 0, 90, 16], np.int32)
+    out = np.array([3, 60, 9, 25, 1, 40], np.int32)
+    BS, Hq, Hkv, D = 8, 8, 2, 128          # more slots than samples: some slots are always empty
+    eng = E.Engine(prompt, out, out, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True,
+                   seed=6)
+    ref = S.simulate(prompt, out, out, BS, eng.num_pages, eng.max_blocks, "lpt", checkpoints=range(0, 10000))
+    done = 0
+    for c in (0, 4, 12, 30, ref.makespan - 1):
+        done += eng.run(c + 1 - done)
+        torch.cuda.synchronize()
+        lens = eng.seq_lens.cpu().numpy()
+        table = eng.block_table.cpu().numpy()
+        assert lens.tolist() == ref.checkpoints[c][0], f"step {c}: lengths"
+        want = oracle.decode_attn(_host_u16(eng.q), _host_u16(eng.k_pages), _host_u16(eng.v_pages), table, lens,
+                                  eng.scale)
+        got = eng.out.float().cpu()
+        for b in range(BS):
+            if lens[b] == 0:
+                assert torch.all(got[b] == 0), f"step {c}: empty slot {b} not cleared"
+        parity.assert_parity(eng.out, want, f"attention at step {c}")
+        eng.out.fill_(float("nan"))      # the caller's write between calls
+    eng.close()
