@@ -341,3 +341,54 @@ def test_max_prefix_batch_one_group():
     ref = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"], case["seq_lens"],
                              case["scale"])
     parity.assert_parity(out, ref, "batch 4096, one group")
+
+
+def _prefix_ws_bytes(B, Hq, Hkv, D, max_blocks, num_pages, ng, workers):
+    import ctypes
+    desc = sl.make_desc(B, Hq, Hkv, D, 16, max_blocks, num_pages, workers, 0)
+    need = ctypes.c_size_t(0)
+    sl._check(sl.load().sl_decode_attn_prefix_workspace_size(ctypes.byref(desc), ng, ctypes.byref(need)), "size")
+    return need.value
+
+
+def test_workspace_contents_and_reuse_do_not_matter():
+    """Nothing the workspace held before may matter: a workspace of random bytes, reused by calls
+    with other batches, group layouts, worker counts and both caches, gives the oracle's rows every
+    time, and repeating a call gives the same bits."""
+    rng = np.random.default_rng(77)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    plan = [(0, 0), (1, 7), (2, 1000), (0, 3), (3, 0)]
+    cases = {}
+    need = 0
+    for case_id, workers in plan:
+        members, prompts, gen, Hq, Hkv, D, extra = CASES[case_id]
+        if case_id not in cases:
+            cases[case_id] = grpo_case(np.random.default_rng(140 + case_id), members, prompts, gen, Hq, Hkv, D,
+                                       extra)
+        case, starts, shared = cases[case_id]
+        B, mb = case["block_table"].shape
+        need = max(need, _prefix_ws_bytes(B, Hq, Hkv, D, mb, case["k_pages"].shape[0], len(shared), workers))
+    b, starts8, shared8 = grpo_fp8_batch(np.random.default_rng(5), [8, 3], [200, 40], 90, 28, 4, 128, extra=2,
+                                         seed=3)
+    need = max(need, _prefix_ws_bytes(b.q.shape[0], 28, 4, 128, b.block_table.shape[1], b.k_pages.shape[0], 2, 0))
+    ws = torch.randint(0, 256, (need + 4096,), dtype=torch.uint8, device=DEV)
+    ws = ws[(-ws.data_ptr()) % 256:][:need]   # 256-byte aligned view of random bytes
+    for case_id, workers in plan:
+        case, starts, shared = cases[case_id]
+        print("workspace reuse: case", case_id, "workers", workers, flush=True)
+        want = oracle.decode_attn(case["q"], case["k_pages"], case["v_pages"], case["block_table"],
+                                  case["seq_lens"], case["scale"])
+        outs = []
+        for rep in range(2):
+            out = sl.decode_attn_prefix(_bf16(case["q"]), _bf16(case["k_pages"]), _bf16(case["v_pages"]),
+                                        d(case["block_table"]), d(case["seq_lens"]), case["scale"], d(starts),
+                                        d(shared), num_workers=workers, workspace=ws)
+            torch.cuda.synchronize()
+            outs.append(out.clone())
+        parity.assert_parity(outs[0], want, f"random workspace, case {case_id}, workers {workers}")
+        assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16)), "repeated call differs"
+    # E4M3 on the same workspace
+    out8 = sl.decode_attn_prefix_fp8(b.q, b.k_pages, b.v_pages, b.k_scales, b.v_scales, b.block_table, b.seq_lens,
+                                     b.scale, starts8, shared8, workspace=ws)
+    torch.cuda.synchronize()
+    parity.assert_parity(out8, parity.oracle_full(b), "E4M3 after the bf16 calls")
