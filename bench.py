@@ -91,9 +91,9 @@ def generation(w, fp8: bool, seed: int, dev) -> dict:
     (lognormal, median 1024, sigma 1, capped at 8192; prompts of 256-768 tokens) on 128 batch
     slots with the workload's head shape. The admission estimate is the true length times a
     lognormal error (sigma 0.3). Runs LPT and FIFO admission; every step is KV append + decode
-    attention for one layer, timed with events around the whole run. With a bf16 cache the
-    engine runs steps with little attention work in one launch; the same two runs with every
-    step as split kernel + merge are reported beside them."""
+    attention for one layer, timed with events around the whole run. The engine runs steps with
+    little attention work in one launch; the same two runs with every step as split kernel +
+    merge are reported beside them."""
     import torch
 
     from paper_2504_15930_amd import engine as E
@@ -105,9 +105,8 @@ def generation(w, fp8: bool, seed: int, dev) -> dict:
     est = np.maximum(1, out * np.exp(rng.normal(0.0, 0.3, M))).astype(np.int32)
     res = {"samples": M, "batch_slots": BS, "output_tokens": int(out.sum()), "max_output": int(out.max()),
            "what": "KV append + decode attention per step, one layer", "kv_dtype": "e4m3" if fp8 else "bf16"}
-    arms = [("lpt", True, False), ("fifo", False, False)]
-    if not fp8:
-        arms += [("lpt_two_launch", True, True), ("fifo_two_launch", False, True)]
+    arms = [("lpt", True, False), ("fifo", False, False), ("lpt_two_launch", True, True),
+            ("fifo_two_launch", False, True)]
     for name, lpt, two in arms:
         print(f"[bench] generation ({name})", file=sys.stderr, flush=True)
         eng = E.Engine(prompt, out, est, batch_slots=BS, num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads,

@@ -31,14 +31,17 @@
  * have length 0 (zero output rows). Within one sl_engine_run call the next
  * step's rows and bookkeeping are written by the launch that finishes this
  * step's attention (after, or beside, its reads of the cache), unless that
- * step admits prompts. With a bf16 cache, a step whose attention fits the chip in one
- * pass of workgroups (at most one workgroup of 8 waves per CU, counting one
- * per (sequence, KV head), and no wave range much longer than a split
- * worker's share) is a single launch: its whole attention, computed in
- * workgroups that combine their own partial states, beside the next step's
- * append (kept in a launch of its own when it would reuse a page freed in
- * this step); other steps run the split kernel, then the merge carrying the
- * next step's append. Every step's output is complete when its launches are.
+ * step admits prompts. A step whose attention fits the chip in one pass of
+ * workgroups (at most one workgroup of 8 waves per CU, counting one per
+ * (sequence, KV head), and no wave range much longer than a split worker's
+ * share) is a single launch: its whole attention, computed in workgroups
+ * that combine their own partial states, and the next step's append (kept in
+ * a launch of its own when it would reuse a page freed in this step). With a
+ * bf16 cache the append runs beside the attention; with an E4M3 cache, whose
+ * append may re-encode a page and raise its scale, each unit's workgroup
+ * appends that unit's row once the unit's reads are done. Other steps run
+ * the split kernel, then the merge carrying the next step's append. Every
+ * step's output is complete when its launches are.
  * When the call's work has completed on desc.stream, the buffers hold the
  * state after its last step.
  *
@@ -50,8 +53,7 @@
  * Memory: all buffers in sl_engine_buffers are the caller's; the engine keeps
  * their pointers until sl_engine_destroy. The engine allocates, at creation
  * only, a small ring of mapped pinned host buffers for its staging and, with
- * a bf16 cache and launch_mode 0, one device buffer (hipMalloc) for the
- * single-launch step: 2048 partial-state slots of G * D accumulator floats
+ * launch_mode 0, one device buffer (hipMalloc) for the single-launch step: 2048 partial-state slots of G * D accumulator floats
  * and G (m, l) pairs (padded to whole 128-byte lines), and 128 * Hkv
  * arrival counters (7.6 MB for G = 7, D = 128). Both are released by
  * sl_engine_destroy.
@@ -77,9 +79,9 @@ typedef struct sl_engine_config {
     const int32_t *prompt_len;  /* host [M], >= 0; read during sl_engine_create only */
     const int32_t *output_len;  /* host [M], >= 1; tokens each sample generates */
     const int32_t *est_len;     /* host [M]; admission key for LPT */
-    int32_t launch_mode;        /* bf16 cache: 0 (default) a step with little attention work runs in one
-                                   launch (attention and the next step's append); 1 every step runs the
-                                   split kernel and the merge. Ignored for an E4M3 cache (always 1). */
+    int32_t launch_mode;        /* 0 (default): a step with little attention work runs in one launch
+                                   (attention and the next step's append); 1: every step runs the split
+                                   kernel and the merge. Either cache type. */
 } sl_engine_config;
 
 typedef struct sl_engine_buffers {

@@ -154,22 +154,16 @@ __device__ __forceinline__ void apply_stage(const AppendParams &p, int first, in
     }
 }
 
-// Append the new rows of unit `unit` = b * Hkv + g (one wavefront). Nothing is
-// appended for an empty sequence; an invalid length or page id leaves the
-// cache untouched. In staged mode the length and the page come from the
-// staging buffer.
+// Append the new rows of unit `unit` = b * Hkv + g (one wavefront) for a
+// sequence of length L (the new token included) whose token L - 1 lives in
+// page `page`. An invalid length or page id leaves the cache untouched.
 template <int D, bool FP8>
-__device__ __forceinline__ void append_unit(const AppendParams &p, int unit, int lane)
+__device__ __forceinline__ void append_row(const AppendParams &p, int unit, int L, int page, int lane)
 {
-    const int b = unit / p.num_kv_heads;
-    const int g = unit - b * p.num_kv_heads;
-    const int L = p.stage ? p.stage[b] : p.seq_lens[b];
-    if (L <= 0 || L > p.max_blocks * kPageSize)
+    if (L <= 0 || L > p.max_blocks * kPageSize || page < 0 || page >= p.num_pages)
         return;
+    const int g = unit % p.num_kv_heads;
     const int t = L - 1;
-    const int page = p.stage ? p.stage[p.batch + b] : p.block_table[(size_t)b * p.max_blocks + t / kPageSize];
-    if (page < 0 || page >= p.num_pages)
-        return;
     const int slot = t % kPageSize;
     const size_t tile = (size_t)page * p.num_kv_heads + g;   // page-head tile index
     const uint16_t *kx = p.k_new + (size_t)unit * D;
@@ -187,6 +181,21 @@ __device__ __forceinline__ void append_unit(const AppendParams &p, int unit, int
         append_e4m3<D>(kx, kt, p.k_scales + tile, slot, lane);
         append_e4m3<D>(vx, vt, p.v_scales + tile, slot, lane);
     }
+}
+
+// Append the new rows of unit `unit` = b * Hkv + g (one wavefront), with the
+// length from the lengths array and the page from the block table, or, in
+// staged mode, both from the staging buffer. Nothing is appended for an
+// empty sequence.
+template <int D, bool FP8>
+__device__ __forceinline__ void append_unit(const AppendParams &p, int unit, int lane)
+{
+    const int b = unit / p.num_kv_heads;
+    const int L = p.stage ? p.stage[b] : p.seq_lens[b];
+    if (L <= 0 || L > p.max_blocks * kPageSize)
+        return;
+    const int page = p.stage ? p.stage[p.batch + b] : p.block_table[(size_t)b * p.max_blocks + (L - 1) / kPageSize];
+    append_row<D, FP8>(p, unit, L, page, lane);
 }
 
 }  // namespace

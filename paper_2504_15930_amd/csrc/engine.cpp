@@ -44,6 +44,7 @@ constexpr int kRing = 8;
 // kUnitSlackTiles tiles of a split-kernel worker's share (the two-launch
 // step spreads tiles over all workers but pays a second launch).
 constexpr int kUnitMinTiles = 1;
+constexpr int kUnitThreads = sl::kUnitWaves * sl::kWave;
 constexpr int kUnitSlackTiles = 8;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
@@ -74,7 +75,7 @@ struct sl_engine {
     bool ev_pending[kRing] = {};
     int ring = 0;
 
-    // One-launch step (bf16): device memory for the pieces and the arrival
+    // One-launch step: device memory for the pieces and the arrival
     // counters, the CU and split-worker counts, which slots' rows are known
     // to be zero, and whether a sample finished in the current step.
     void *unit_mem = nullptr;
@@ -322,6 +323,16 @@ sl_status sl_engine::one_step(bool chain)
     const bool one_launch = plan_unit_step(cur);
     if (one_launch && freed_now && next.n_upd > 0)
         fuse = false;
+    // E4M3: the units append their own next-step rows after their reads, so
+    // every slot the next step appends to must be one of this step's (a
+    // prompt of length 0 admits a sample without filling pages).
+    if (one_launch && fp8 && fuse) {
+        const int32_t *hc = h_stage[cur.ring], *hn = h_stage[next.ring];
+        for (int b = 0; b < BS && fuse; ++b)
+            fuse = hn[b] <= 0 || (hc[b] > 0 && hn[b] == hc[b] + 1);
+        for (int e = 0; e < up.n_entries; ++e)
+            up.next_page[e] = hn[up.seq[e]] > 0 ? hn[BS + up.seq[e]] : -1;
+    }
     if (chain && !last) {
         next_state = fuse ? kLaunched : kPrepared;
         if (fuse) {
@@ -331,8 +342,14 @@ sl_status sl_engine::one_step(bool chain)
     }
     if (one_launch) {
         up.next = fused ? *fused : sl::AppendParams{};
-        up.next_blocks = fused ? (BS * Hkv + sl::kUnitWaves - 1) / sl::kUnitWaves : 0;
-        if (sl::launch_unit_step(up, D, step_desc.stream) != hipSuccess)
+        up.units_append = fused && fp8;
+        if (!fused)
+            up.next_blocks = 0;
+        else if (fp8)   // the bookkeeping only: BS lengths and the table updates
+            up.next_blocks = (std::max(BS, next.n_upd) + kUnitThreads - 1) / kUnitThreads;
+        else            // and a wave per (slot, KV head) append
+            up.next_blocks = (BS * Hkv + sl::kUnitWaves - 1) / sl::kUnitWaves;
+        if (sl::launch_unit_step(up, D, fp8, step_desc.stream) != hipSuccess)
             return SL_ERR_HIP;
         for (int e = 0; e < up.n_entries; ++e)
             zeroed[up.seq[e]] = 0;
@@ -448,10 +465,10 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     // staging: lengths, token pages, at most BS * (prompt blocks + 1) updates, BS * prompt blocks fills
     e->stage_ints = 2 * (size_t)BS + 3 * (size_t)BS * (max_prompt_blocks + 1) + (size_t)BS * max_prompt_blocks;
     e->zeroed.assign(BS, 0);
-    // One-launch step (bf16): piece slots (kMaxUnitBlocks workgroups, each G
-    // pairs (m, l) on whole cache lines and G rows of D accumulators) and the
+    // One-launch step: piece slots (kMaxUnitBlocks workgroups, each G pairs
+    // (m, l) on whole cache lines and G rows of D accumulators) and the
     // arrival counters, zeroed.
-    if (!fp8 && cfg->launch_mode == 0) {
+    if (cfg->launch_mode == 0) {
         const int G = d.num_q_heads / d.num_kv_heads;
         int dev = 0, nw = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -459,7 +476,7 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
             delete e;
             return SL_ERR_HIP;
         }
-        st = sl_decode_attn_num_workers(&d, 0, &nw);
+        st = sl_decode_attn_num_workers(&d, fp8 ? 1 : 0, &nw);
         if (st != SL_OK) {
             delete e;
             return st;
@@ -484,8 +501,8 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
         sp.q = bufs->q;
         sp.k_pages = bufs->k_pages;
         sp.v_pages = bufs->v_pages;
-        sp.k_scales = nullptr;
-        sp.v_scales = nullptr;
+        sp.k_scales = fp8 ? bufs->k_scales : nullptr;
+        sp.v_scales = fp8 ? bufs->v_scales : nullptr;
         sp.out = bufs->out;
         sp.part_ml = reinterpret_cast<float *>(base);
         sp.part_acc = reinterpret_cast<float *>(base + ml_bytes);

@@ -69,13 +69,18 @@ __global__ __launch_bounds__(kEngineThreads) void engine_fill_kernel(const int32
 // product, whatever they hold), its table entries are past the ones read,
 // and the host keeps the append in a launch of its own when it would reuse a
 // page this step reads (a page freed by a sequence that finished in it).
+// An E4M3 append may also re-encode the earlier rows of that page and raise
+// its scale; there the unit's own workgroup appends the unit's row once all
+// of the unit's reads are done (units_append), and next_blocks only apply
+// the bookkeeping.
 
 constexpr int kUnitThreads = kUnitWaves * kWave;
-constexpr int kUnitDepth = 2;   // tiles in flight per wave
+template <bool FP8>
+constexpr int unit_depth() { return FP8 ? 3 : 2; }   // tiles in flight per wave (as the split kernel)
 
-// LDS of an attention workgroup: the waves' K regroup stages, then every
-// wave's final state, lane-major (D / 4 accumulator values, m and l per
-// lane): 100 KB for D = 128, which gfx950's 160 KB of LDS per CU holds (the
+// LDS of an attention workgroup: the waves' K regroup stages (sized for
+// bf16 tiles, which E4M3 tiles fit), then every wave's final state,
+// lane-major (D / 4 accumulator values, m and l per lane): 100 KB for D = 128, which gfx950's 160 KB of LDS per CU holds (the
 // kernel's registers allow one such workgroup per CU anyway).
 template <int D>
 constexpr int unit_state_floats() { return D / 4 + 2; }
@@ -110,7 +115,7 @@ __device__ __forceinline__ f32x2_t load2_device(__amdgpu_buffer_rsrc_t r, int of
     return __builtin_bit_cast(f32x2_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCachePolicyDevice));
 }
 
-template <int D>
+template <int D, bool FP8>
 __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk, uint8_t *smem, int32_t *s_last)
 {
     const SplitParams &p = up.cur;
@@ -164,7 +169,7 @@ __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk
             const uint16_t *qrow = p.q + ((size_t)row0 + (size_t)min(n, G - 1)) * D;
 #pragma unroll
             for (int s = 0; s < D / 32; ++s) {
-                const u32x4_t x = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, false>(s, quad)));
+                const u32x4_t x = ld128(reinterpret_cast<const uint8_t *>(qrow + q_index<D, FP8>(s, quad)));
                 qop[s] = __builtin_bit_cast(bf16x8_t, n < G ? x : u32x4_t{0u, 0u, 0u, 0u});
             }
         }
@@ -177,27 +182,28 @@ __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk
             const int live = min(kPageSize, Lc - (t0 + i) * kPageSize);   // >= 1: t0 + i < nb
             return (uint32_t)(live - 1) | (row0 << kMetaRowShift);
         };
-        // kUnitDepth tiles in flight.
-        Tile<D, false> buf[kUnitDepth];
+        // kDepth tiles in flight.
+        constexpr int kDepth = unit_depth<FP8>();
+        Tile<D, FP8> buf[kDepth];
 #pragma unroll
-        for (int k0 = 0; k0 < kUnitDepth - 1; ++k0)
+        for (int k0 = 0; k0 < kDepth - 1; ++k0)
             if (k0 < nt)
-                issue_tile<D, false>(buf[k0], p, page_at(k0), meta_at(k0), false, n, quad, lane);
-        for (int i0 = 0; i0 < nt; i0 += kUnitDepth) {
+                issue_tile<D, FP8>(buf[k0], p, page_at(k0), meta_at(k0), false, n, quad, lane);
+        for (int i0 = 0; i0 < nt; i0 += kDepth) {
 #pragma unroll
-            for (int kk = 0; kk < kUnitDepth; ++kk) {
+            for (int kk = 0; kk < kDepth; ++kk) {
                 const int i = i0 + kk;
                 if (i < nt) {
-                    const int ia = i + kUnitDepth - 1;   // the tile issued now
+                    const int ia = i + kDepth - 1;   // the tile issued now
                     if (ia < nt) {
                         if ((ia & (kWave - 1)) == 0)     // the next 64 entries
                             ids = lane < nt - ia ? bt_row[ia + lane] : 0;
-                        issue_tile<D, false>(buf[(kk + kUnitDepth - 1) % kUnitDepth], p, page_at(ia), meta_at(ia),
-                                             false, n, quad, lane);
+                        issue_tile<D, FP8>(buf[(kk + kDepth - 1) % kDepth], p, page_at(ia), meta_at(ia), false, n,
+                                           quad, lane);
                     }
-                    const Tile<D, false> &t = buf[kk];
+                    const Tile<D, FP8> &t = buf[kk];
                     bad |= t.bad_page;
-                    compute_tile<D, false>(st, t, qop, p.scale_log2, (int)(t.meta & 15u) + 1, lds, lane, n, quad);
+                    compute_tile<D, FP8>(st, t, qop, p.scale_log2, (int)(t.meta & 15u) + 1, lds, lane, n, quad);
                 }
             }
         }
@@ -286,8 +292,16 @@ __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk
                 store2_device(ml_rsrc, 4 * (blk * mls + 2 * cn), f32x2_t{M + poison, L});
         }
     }
-    if (K == 1)
+    // The unit's next-step row, by the last wave (which has no combine work
+    // for any G <= 16: the combine takes threads below 16 G): with one
+    // workgroup per unit, every wave's reads of the unit's pages are done
+    // once the barrier above has passed.
+    const bool tail_append = up.units_append && wave == kUnitWaves - 1;
+    if (K == 1) {
+        if (tail_append)
+            append_row<D, FP8>(up.next, b * Hkv + g, L + 1, up.next_page[e], lane);
         return;
+    }
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);   // this wave's part of the piece has reached the coherent level
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -297,6 +311,10 @@ __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk
     __syncthreads();
     if (*s_last == 0)
         return;
+    // Every workgroup of the unit has counted its arrival after its loads
+    // returned, so none reads the unit's pages any more.
+    if (tail_append)
+        append_row<D, FP8>(up.next, b * Hkv + g, L + 1, up.next_page[e], lane);
     // The last arrival merges the unit's K pieces (slots first[e] + g K ..),
     // in slot order, row j and four columns per thread. Up to eight pieces:
     // every load at once; more: the (m, l) pairs through LDS first, then
@@ -372,14 +390,14 @@ __device__ __forceinline__ void unit_attention(const UnitStepParams &up, int blk
         __hip_atomic_store(up.counters + unit, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(kUnitThreads) void engine_unit_step_kernel(UnitStepParams up)
 {
     __shared__ __attribute__((aligned(16))) uint8_t smem[unit_smem_bytes<D>()];
     __shared__ int32_t s_last;
     int blk = (int)blockIdx.x;
     if (blk < up.unit_blocks) {
-        unit_attention<D>(up, blk, smem, &s_last);
+        unit_attention<D, FP8>(up, blk, smem, &s_last);
         return;
     }
     blk -= up.unit_blocks;
@@ -391,22 +409,28 @@ __global__ __launch_bounds__(kUnitThreads) void engine_unit_step_kernel(UnitStep
     }
     blk -= up.zero_blocks;
     apply_stage(up.next, blk * kUnitThreads + (int)threadIdx.x, up.next_blocks * kUnitThreads);
+    if (up.units_append)
+        return;
     const int unit = blk * kUnitWaves + (int)(threadIdx.x / kWave);
     if (unit < up.next.batch * up.next.num_kv_heads)
-        append_unit<D, false>(up.next, unit, threadIdx.x & (kWave - 1));
+        append_unit<D, FP8>(up.next, unit, threadIdx.x & (kWave - 1));
 }
 
 }  // namespace
 
-hipError_t launch_unit_step(const UnitStepParams &up, int head_dim, hipStream_t stream)
+hipError_t launch_unit_step(const UnitStepParams &up, int head_dim, bool fp8, hipStream_t stream)
 {
-    const dim3 grid((unsigned)(up.unit_blocks + up.zero_blocks + up.next_blocks));
+    const dim3 grid((unsigned)(up.unit_blocks + up.zero_blocks + up.next_blocks)), block(kUnitThreads);
     if (grid.x == 0)
         return hipSuccess;
-    if (head_dim == 128)
-        hipLaunchKernelGGL(engine_unit_step_kernel<128>, grid, dim3(kUnitThreads), 0, stream, up);
-    else if (head_dim == 64)
-        hipLaunchKernelGGL(engine_unit_step_kernel<64>, grid, dim3(kUnitThreads), 0, stream, up);
+    if (head_dim == 128 && !fp8)
+        hipLaunchKernelGGL((engine_unit_step_kernel<128, false>), grid, block, 0, stream, up);
+    else if (head_dim == 64 && !fp8)
+        hipLaunchKernelGGL((engine_unit_step_kernel<64, false>), grid, block, 0, stream, up);
+    else if (head_dim == 128 && fp8)
+        hipLaunchKernelGGL((engine_unit_step_kernel<128, true>), grid, block, 0, stream, up);
+    else if (head_dim == 64 && fp8)
+        hipLaunchKernelGGL((engine_unit_step_kernel<64, true>), grid, block, 0, stream, up);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -66,8 +66,8 @@ class Engine:
 
     Allocates (with torch) the page pool, block table, lengths, query and
     new-row buffers, output and workspace; ``q``/``k_new``/``v_new`` hold
-    seeded random rows used in every step. ``two_launch`` makes every bf16
-    step run the split kernel and the merge; ``history_steps`` > 0 keeps the
+    seeded random rows used in every step. ``two_launch`` makes every step
+    run the split kernel and the merge; ``history_steps`` > 0 keeps the
     outputs of the first that many steps in ``history``.
     """
 

@@ -31,14 +31,14 @@ def _case(seed, M, lo_p=0, hi_p=100, med_o=40):
     return prompt, out, est
 
 
-@pytest.mark.parametrize("mode", ["bf16", "bf16-two-launch", "e4m3"])
+@pytest.mark.parametrize("mode", ["bf16", "bf16-two-launch", "e4m3", "e4m3-two-launch"])
 @pytest.mark.parametrize("lpt", [True, False], ids=["lpt", "fifo"])
 def test_engine_matches_oracle(lpt, mode):
-    fp8 = mode == "e4m3"
+    fp8 = mode.startswith("e4m3")
     prompt, out, est = _case(11 if lpt else 12, M=30)
     BS, Hq, Hkv, D = 6, 8, 2, 128
     eng = E.Engine(prompt, out, est, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D,
-                   kv_fp8=fp8, lpt=lpt, seed=3, two_launch=mode == "bf16-two-launch")
+                   kv_fp8=fp8, lpt=lpt, seed=3, two_launch=mode.endswith("two-launch"))
     ref = S.simulate(prompt, out, est, BS, eng.num_pages, eng.max_blocks, "lpt" if lpt else "fifo",
                      checkpoints=range(0, 10000))
     checks = [0, 1, 2, 7, 16, 33, ref.makespan // 2, ref.makespan - 1]
@@ -128,13 +128,16 @@ def test_engine_one_launch_long_contexts():
 
 @pytest.mark.parametrize("queries", ["zero", "random"])
 @pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 128), (16, 1, 64)], ids=["G4-D128", "G16-D64"])
-def test_engine_one_launch_every_step_matches_two_launch(Hq, Hkv, D, queries):
+@pytest.mark.parametrize("kv", ["bf16", "e4m3"])
+def test_engine_one_launch_every_step_matches_two_launch(kv, Hq, Hkv, D, queries):
     """Every step's output of a whole generation, kept in the engine's output history, with one
     launch per step against split + merge (whose steps the oracle checks above). The samples finish
     often, open pages often (prompts of 0, 16, 32 tokens among them) and include one 3000-token
     prompt, so the steps cover units of one and of many workgroups, empty slots, admissions beside
     finishes, and next-step appends that take a page freed in the same step (those run in a launch
-    of their own).
+    of their own). With an E4M3 cache the one-launch step's units append their own next rows (the
+    single workgroup of a unit, or the last of its workgroups to arrive); both runs must leave the
+    same codes and scales in every page, bit for bit.
 
     Zero queries make every weight exactly 1: both paths then compute the mean of the value rows
     and may differ only in the last place of the bf16 output, while a row read at the wrong time
@@ -150,18 +153,23 @@ def test_engine_one_launch_every_step_matches_two_launch(Hq, Hkv, D, queries):
     ref = S.simulate(prompt, out, out, BS, BS * int(((prompt + out + 15) // 16).max()),
                      int(((prompt + out + 15) // 16).max()), "lpt")
     steps = ref.makespan
-    hist = {}
-    vmax = 2.0   # synthetic prompt values are uniform in [-2, 2)
+    hist, cache = {}, {}
+    vmax = 2.0   # synthetic prompt values lie in (-2, 2) for both caches
     for two in (False, True):
         eng = E.Engine(prompt, out, out, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True,
-                       seed=9, two_launch=two, history_steps=steps)
+                       kv_fp8=kv == "e4m3", seed=9, two_launch=two, history_steps=steps)
         if queries == "zero":
             eng.q.zero_()
         vmax = max(vmax, float(eng.v_new.float().abs().max()))
         assert eng.run() == steps
         torch.cuda.synchronize()
         hist[two] = eng.history.float().cpu()
+        cache[two] = [t.cpu().view(torch.uint8) if t.dtype != torch.float32 else t.cpu().view(torch.int32)
+                      for t in ((eng.k_pages, eng.v_pages, eng.k_scales, eng.v_scales) if kv == "e4m3"
+                                else (eng.k_pages, eng.v_pages))]
         eng.close()
+    for x, y, name in zip(cache[False], cache[True], ("k pages", "v pages", "k scales", "v scales")):
+        assert torch.equal(x, y), f"{name} differ between the launch modes"
     a, b = hist[False], hist[True]
     assert torch.isfinite(a).all() and torch.isfinite(b).all()
     mag = torch.maximum(a.abs(), b.abs()).clamp_min(2.0 ** -126)
