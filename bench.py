@@ -49,6 +49,10 @@ KERNEL_SOURCES = ["paper_2504_15930_amd/csrc/decode_split.hip", "paper_2504_1593
 OTHER_CONFIGS = ["straggler", "qwen72b_longtail", "fp8_qwen7b_longtail"]
 TARGET_PCT = {"qwen7b_longtail": 75.0, "qwen72b_longtail": 75.0, "straggler": 60.0, "fp8_qwen7b_longtail": None}
 MODEL_LAYERS = {"qwen7b_longtail": 28, "fp8_qwen7b_longtail": 28, "qwen72b_longtail": 80, "straggler": 80}
+# bf16 weights a whole model's decode step reads once (every decode step touches all parameters,
+# Section 2.2): Qwen2.5-7B holds about 7.6 B parameters, Qwen2.5-72B about 72.7 B.
+MODEL_WEIGHT_BYTES = {"qwen7b_longtail": 15.2e9, "fp8_qwen7b_longtail": 15.2e9, "qwen72b_longtail": 145.4e9,
+                      "straggler": 145.4e9}
 
 
 def algorithmic_bytes(seq_lens: np.ndarray, num_q_heads: int, num_kv_heads: int, head_dim: int,
@@ -141,10 +145,10 @@ def ptl_at(batch: int, prof_b, prof_s) -> float:
     return ys[-1] + (ys[-1] - ys[-2]) * (batch - xs[-1]) / (xs[-1] - xs[-2])
 
 
-DISPATCH_REGIMES = [(1024, 128), (1024, 32), (4096, 128)]   # (prompts, most sequences an instance decodes at once)
+DISPATCH_REGIMES = [(1024, 128), (1024, 32), (4096, 128), (4096, 32)]   # (prompts, most decoded at once)
 
 
-def dispatch_experiment(w, seed: int, dev) -> dict:
+def dispatch_experiment(w, seed: int, dev, stream_gbs: float | None = None) -> dict:
     """Skewness-aware dispatching (Algorithm 2 with Equation 2) fed by PTL(BS) measured here,
     against random dispatching, with the generation stage of every plan run on the decode engine.
 
@@ -160,8 +164,15 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
     the plan, and Sum over steps of PTL(sequences active in that step) along the slowest instance's
     actual schedule. The regimes: 1024 prompts with 128 per instance at once (a random instance
     holds 128 prompts: one round), and with 32 (four rounds), the case Equation 2's ceil(M / BS)
-    and the paper's scheduling-order discussion are about; and 4096 prompts with 128 at once (a
-    random instance holds 512 prompts: four rounds)."""
+    and the paper's scheduling-order discussion are about; 4096 prompts with 128 at once (a random
+    instance holds 512 prompts: four rounds); and 4096 prompts with 32 at once (sixteen rounds, so
+    that an instance's steps are set by its total output rather than by its longest sample).
+
+    With ``stream_gbs`` (this GPU's measured streaming rate) every plan also gets a modelled
+    whole-model stage: per instance, its measured one-layer time times the model's layer count,
+    plus its step count times the time to stream the model's bf16 weights once at that rate (the
+    per-step floor that a whole model's decode step has and attention alone lacks); the stage is
+    the slowest instance."""
     import torch
 
     from paper_2504_15930_amd import dispatch as Dsp
@@ -192,6 +203,14 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
     res = {"ptl_profile": {"batch": prof_b, "us": [round(x * 1e6, 2) for x in prof_s],
                            "what": "KV append + decode attention, 2048 cached tokens per sequence"},
            "instances": N, "alpha": alpha, "estimate_error_sigma": 0.3, "regimes": []}
+    layers = MODEL_LAYERS.get(w.name)
+    weight_ms = None
+    if stream_gbs and layers and w.name in MODEL_WEIGHT_BYTES:
+        weight_ms = MODEL_WEIGHT_BYTES[w.name] / (stream_gbs * 1e9) * 1e3
+        res["whole_model"] = {"layers": layers, "weight_bytes": MODEL_WEIGHT_BYTES[w.name],
+                              "stream_GBps": round(stream_gbs, 1), "weight_ms_per_step": round(weight_ms, 4),
+                              "what": "per instance: layers x its measured one-layer time + its steps x the "
+                                      "time to stream the weights once; stage = slowest instance"}
 
     for P, maxb in DISPATCH_REGIMES:
         rng = np.random.default_rng(seed)
@@ -202,12 +221,13 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
 
         def run_plan(inst, order_len):
             """Every instance of a plan on the engine; its slowest instance is the stage time."""
-            per, sched = [], []
+            per, sched, steps = [], [], []
             for k in range(N):
                 idx = np.nonzero(inst == k)[0]
                 if len(idx) == 0:
                     per.append(0.0)
                     sched.append(0.0)
+                    steps.append(0)
                     continue
                 eng = E.Engine(prompt[idx], true[idx], order_len[idx], batch_slots=min(len(idx), maxb),
                                num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True, seed=seed, device=dev)
@@ -217,16 +237,20 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
                 eng.run()
                 e1.record()
                 torch.cuda.synchronize()
-                active = eng.schedule()[4]
+                n_steps, active = eng.schedule()[3:5]
                 per.append(round(e0.elapsed_time(e1), 2))
                 sched.append(round(1e3 * sum(ptl_at(int(a), prof_b, prof_s) for a in active), 2))
+                steps.append(int(n_steps))
                 eng.close()
                 del eng
                 torch.cuda.empty_cache()
             k = int(np.argmax(per))
-            return {"stage_ms": per[k], "instance_ms": per, "slowest_instance": k,
-                    "slowest_prompts": int((inst == k).sum()), "slowest_longest_output": int(true[inst == k].max()),
-                    "schedule_ptl_estimate_ms": sched[k]}
+            r = {"stage_ms": per[k], "instance_ms": per, "instance_steps": steps, "slowest_instance": k,
+                 "slowest_prompts": int((inst == k).sum()), "slowest_longest_output": int(true[inst == k].max()),
+                 "schedule_ptl_estimate_ms": sched[k]}
+            if weight_ms is not None:
+                r["whole_model_stage_ms"] = round(max(layers * t + n * weight_ms for t, n in zip(per, steps)), 1)
+            return r
 
         reg = {"prompts": P, "max_batch": maxb}
         print(f"[bench] dispatch {P} prompts, {maxb} at once: random", file=sys.stderr, flush=True)
@@ -244,6 +268,9 @@ def dispatch_experiment(w, seed: int, dev) -> dict:
                 r = dict(done[(nl, nr)])
                 r.update(long_tail_instances=nl, regular_instances=nr, eq2_estimate_ms=round(lat * 1e3, 2),
                          speedup_over_random=round(reg["random"]["stage_ms"] / max(r["stage_ms"], 1e-9), 3))
+                if weight_ms is not None:
+                    r["whole_model_speedup_over_random"] = round(
+                        reg["random"]["whole_model_stage_ms"] / max(r["whole_model_stage_ms"], 1e-9), 3)
                 reg[f"{arm}_{combine}"] = r
         res["regimes"].append(reg)
     return res
@@ -743,7 +770,7 @@ def main(argv=None) -> int:
     if args.generation:
         result["generation"] = generation(w, kvb == 1, args.seed, dev)
     if args.dispatch:
-        result["dispatch"] = dispatch_experiment(w, args.seed, dev)
+        result["dispatch"] = dispatch_experiment(w, args.seed, dev, stream_gbs=result["roofline"]["achieved"])
     print(json.dumps(result), flush=True)
     return 0
 
