@@ -38,7 +38,16 @@
 namespace {
 
 using sl::kPageSize;
+// Staging ring: kRing mapped pinned buffers, taken in order. The host may
+// rewrite a buffer only after the kernels that read it have finished. An
+// event is recorded after the launch that reads the last buffer of each
+// group of kRingGroup (launches read the buffers in ring order, on one
+// stream), so one event covers the whole group and the host still runs at
+// least kRing - kRingGroup steps ahead: recording one after every launch
+// left the device idle for ~5 us before each step's first kernel.
 constexpr int kRing = 8;
+constexpr int kRingGroup = 4;
+constexpr int kRingEvents = kRing / kRingGroup;
 // One-launch step: a wave gets at least this many tiles of its unit, and the
 // step takes the one-launch path only while its longest wave range is within
 // kUnitSlackTiles tiles of a split-kernel worker's share (the two-launch
@@ -71,8 +80,8 @@ struct sl_engine {
     size_t stage_ints = 0;
     int32_t *h_stage[kRing] = {};   // mapped pinned staging buffers
     int32_t *d_stage[kRing] = {};   // their device addresses
-    hipEvent_t ev[kRing] = {};
-    bool ev_pending[kRing] = {};
+    hipEvent_t ev[kRingEvents] = {};    // one per group of kRingGroup buffers
+    bool ev_pending[kRingEvents] = {};
     int ring = 0;
 
     // One-launch step: device memory for the pieces and the arrival
@@ -86,12 +95,12 @@ struct sl_engine {
 
     void release()
     {
-        for (int r = 0; r < kRing; ++r) {
-            if (ev[r])
-                (void)hipEventDestroy(ev[r]);
+        for (int k = 0; k < kRingEvents; ++k)
+            if (ev[k])
+                (void)hipEventDestroy(ev[k]);
+        for (int r = 0; r < kRing; ++r)
             if (h_stage[r])
                 (void)hipHostFree(h_stage[r]);
-        }
         if (unit_mem)
             (void)hipFree(unit_mem);
     }
@@ -106,6 +115,7 @@ struct sl_engine {
     Staged next;
 
     sl_status prepare(Staged &out);
+    sl_status staged_launched(int r, hipStream_t s);
     sl::AppendParams append_params(const Staged &sg) const;
     sl_status launch_staged(const Staged &sg);
     bool plan_unit_step(const Staged &sg);
@@ -145,9 +155,10 @@ sl_status sl_engine::prepare(Staged &out)
     // for every token that opens one.
     const int r = ring;
     ring = (ring + 1) % kRing;
-    if (ev_pending[r] && hipEventSynchronize(ev[r]) != hipSuccess)
+    const int grp = r / kRingGroup;   // its group's event, recorded a lap ago, covers its last use
+    if (ev_pending[grp] && hipEventSynchronize(ev[grp]) != hipSuccess)
         return SL_ERR_HIP;
-    ev_pending[r] = false;
+    ev_pending[grp] = false;
     int32_t *h = h_stage[r];
     for (int b = 0; b < BS; ++b) {
         const int i = occupant[b];
@@ -207,9 +218,18 @@ sl_status sl_engine::launch_staged(const Staged &sg)
         return SL_ERR_HIP;
     if (sl::launch_append(append_params(sg), D, fp8, s) != hipSuccess)
         return SL_ERR_HIP;
-    if (hipEventRecord(ev[sg.ring], s) != hipSuccess)   // the staging buffer is free again after this
+    return staged_launched(sg.ring, s);
+}
+
+// The launch that reads staging buffer r has been enqueued on s: after the
+// last buffer of a group, record the group's event.
+sl_status sl_engine::staged_launched(int r, hipStream_t s)
+{
+    if (r % kRingGroup != kRingGroup - 1)
+        return SL_OK;
+    if (hipEventRecord(ev[r / kRingGroup], s) != hipSuccess)
         return SL_ERR_HIP;
-    ev_pending[sg.ring] = true;
+    ev_pending[r / kRingGroup] = true;
     return SL_OK;
 }
 
@@ -375,11 +395,8 @@ sl_status sl_engine::one_step(bool chain)
                            hipMemcpyDeviceToDevice, step_desc.stream) != hipSuccess)
             return SL_ERR_HIP;
     }
-    if (fused) {
-        if (hipEventRecord(ev[next.ring], step_desc.stream) != hipSuccess)
-            return SL_ERR_HIP;
-        ev_pending[next.ring] = true;
-    }
+    if (fused && (st = staged_launched(next.ring, step_desc.stream)) != SL_OK)
+        return st;
     if (last)
         done = true;
     return SL_OK;
@@ -525,8 +542,9 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     for (int r = 0; ok && r < kRing; ++r)
         ok = hipHostMalloc(reinterpret_cast<void **>(&e->h_stage[r]), sizeof(int32_t) * e->stage_ints,
                            hipHostMallocMapped) == hipSuccess &&
-             hipHostGetDevicePointer(reinterpret_cast<void **>(&e->d_stage[r]), e->h_stage[r], 0) == hipSuccess &&
-             hipEventCreateWithFlags(&e->ev[r], hipEventDisableTiming) == hipSuccess;
+             hipHostGetDevicePointer(reinterpret_cast<void **>(&e->d_stage[r]), e->h_stage[r], 0) == hipSuccess;
+    for (int k = 0; ok && k < kRingEvents; ++k)
+        ok = hipEventCreateWithFlags(&e->ev[k], hipEventDisableTiming) == hipSuccess;
     if (!ok) {
         e->release();
         delete e;
