@@ -283,8 +283,9 @@ sl_status sl_decode_attn_noalloc(const sl_attn_desc *desc, const uint16_t *q,
                                  const int32_t *block_table, const int32_t *seq_lens,
                                  float scale, uint16_t *out);
 
-/* Static English description of a status code (never NULL). */
-const char *sl_status_string(sl_status status);
+/* Static English description of a status code (never NULL). Takes any
+ * integer: a value that is no sl_status gives "unknown status". */
+const char *sl_status_string(int32_t status);
 
 #ifdef __cplusplus
 }

@@ -34,9 +34,10 @@ def _hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(output: str = LIBRARY, extra: list[str] | None = None, verbose: bool = False) -> str:
+def build(output: str = LIBRARY, extra: list[str] | None = None, verbose: bool = False,
+          objdir: str | None = None) -> str:
     """Compile every source and link ``output``; returns its path."""
-    objdir = os.path.join(HERE, "_build")
+    objdir = objdir or os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     flags = HIPCC_FLAGS + list(extra or [])
 
@@ -58,6 +59,29 @@ def build(output: str = LIBRARY, extra: list[str] | None = None, verbose: bool =
     subprocess.run(cmd, check=True)
     os.replace(tmp, output)
     return output
+
+
+# The whole library with its host code (the C ABI, the engine's host loop, dispatching)
+# under the sanitizers and its GPU code unchanged: every flag applies to the host pass only.
+HOST_SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                       "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer",
+                       "-Xarch_host", "-g"]
+
+
+# UBSan alone, for runs that use the GPU: ROCm's ASan runtime intercepts the HSA allocator for
+# device-side checking, which cannot run here, so a process that touches the GPU takes no ASan.
+HOST_UBSAN_FLAGS = ["-Xarch_host", "-fsanitize=undefined", "-Xarch_host", "-fno-sanitize=vptr",
+                    "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-g"]
+
+
+def clang_runtime(name: str) -> str | None:
+    """A sanitizer runtime of the compiler hipcc drives (``asan`` or ``ubsan_standalone``), to
+    preload into an uninstrumented Python."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    import glob
+    hits = sorted(glob.glob(os.path.join(rocm, "llvm", "lib", "clang", "*", "lib", "linux",
+                                         f"libclang_rt.{name}-x86_64.so")))
+    return hits[-1] if hits else None
 
 
 # Host-only build of the dispatching code (csrc/dispatch.cpp, no GPU code) with the host

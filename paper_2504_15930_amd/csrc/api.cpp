@@ -493,7 +493,7 @@ sl_status sl_decode_attn_fp8(const sl_attn_desc *desc, const uint16_t *q, const 
                    out, true);
 }
 
-const char *sl_status_string(sl_status status)
+const char *sl_status_string(int32_t status)
 {
     switch (status) {
     case SL_OK: return "success";

@@ -180,8 +180,10 @@ sl_status sl_engine::prepare(Staged &out)
     out.ring = r;
     out.n_upd = (int)upd.size() / 3;
     out.n_fill = (int)fills.size();
-    std::memcpy(h + 2 * BS, upd.data(), sizeof(int32_t) * upd.size());
-    std::memcpy(h + 2 * BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
+    if (!upd.empty())   // (an empty vector's data() may be null, which memcpy must not get)
+        std::memcpy(h + 2 * BS, upd.data(), sizeof(int32_t) * upd.size());
+    if (!fills.empty())
+        std::memcpy(h + 2 * BS + upd.size(), fills.data(), sizeof(int32_t) * fills.size());
     return SL_OK;
 }
 

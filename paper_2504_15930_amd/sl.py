@@ -13,7 +13,8 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIBRARY = os.path.join(HERE, "libsl.so")
+# SL_LIBRARY may name another build of the same sources (the host-sanitized one of the tests).
+LIBRARY = os.environ.get("SL_LIBRARY") or os.path.join(HERE, "libsl.so")
 
 SL_OK = 0
 STATUS_NAMES = {0: "SL_OK", -1: "SL_ERR_NULL", -2: "SL_ERR_SHAPE", -3: "SL_ERR_UNSUPPORTED",
@@ -79,7 +80,7 @@ def load(path: str = LIBRARY) -> ctypes.CDLL:
     lib.sl_decode_attn_prefix_workspace_size.argtypes = [D, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
     lib.sl_kv_append_fp8.argtypes = [D, P, P, P, P, P, P, P, P]
     lib.sl_decode_attn_noalloc.argtypes = [D, P, P, P, P, P, ctypes.c_float, P]
-    lib.sl_status_string.argtypes = [ctypes.c_int]
+    lib.sl_status_string.argtypes = [ctypes.c_int32]
     lib.sl_status_string.restype = ctypes.c_char_p
     for name in EXPORTS[:-1]:
         getattr(lib, name).restype = ctypes.c_int
