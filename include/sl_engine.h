@@ -132,7 +132,9 @@ sl_status sl_engine_schedule(const sl_engine *engine, int32_t *slot, int32_t *ad
                              int32_t *finish_step, int32_t *steps, int32_t *active,
                              int32_t active_cap);
 
-/* Wait for the engine's stream, then release its staging memory. NULL is a no-op. */
+/* Wait for the engine's stream, then release its staging memory. NULL is a no-op.
+ * (Calls on one engine must not overlap: one host thread at a time. Separate
+ * engines share nothing.) */
 sl_status sl_engine_destroy(sl_engine *engine);
 
 #ifdef __cplusplus
