@@ -1,6 +1,7 @@
 """sl_decode_attn_noalloc (the entry point that allocates nothing) against sl_decode_attn and the
 oracle, through the C ABI: two calls in a row on the library's fixed scratch array, the second on
-a smaller batch, then the 7B-like long-tail batch at full size with the default worker count."""
+a smaller batch, then the 7B-like long-tail batch at full size with the default worker count, and
+replays of a call captured in a HIP graph."""
 import numpy as np
 import pytest
 import torch
@@ -64,3 +65,31 @@ def test_scratch_limit_rejected_before_launch():
     assert e.value.status == -7
     torch.cuda.synchronize()
     assert bool((out.float() == 7.0).all()), "a rejected call enqueued work"
+
+
+def test_replays_of_a_captured_call():
+    """The use the entry point exists for: one call captured in a HIP graph (through torch's graph
+    capture, after one eager call that looks up the scratch address), replayed five times with eager
+    work between the replays (the queries rewritten, an unrelated call on a workspace); every replay
+    equals sl_decode_attn on the same inputs, bit for bit."""
+    rng = np.random.default_rng(5)
+    lens = np.clip(np.exp(rng.normal(np.log(500), 1.0, 40)), 1, 3000).astype(np.int64)
+    b = inputs.make_paged_batch(lens, 28, 4, 128, seed=6, device=DEV, poison=False)
+    other = inputs.make_paged_batch(rng.integers(1, 900, 12), 16, 2, 64, seed=7, device=DEV, poison=False)
+    out = torch.empty_like(b.q)
+    sl.decode_attn_noalloc(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, out=out)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sl.decode_attn_noalloc(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale, out=out)
+    gen = torch.Generator(device=DEV).manual_seed(8)
+    for r in range(5):
+        print("graph replay", r, flush=True)
+        b.q.copy_(torch.randn(b.q.shape, generator=gen, device=DEV).to(torch.bfloat16))
+        sl.run_batch(other)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        want = sl.decode_attn(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale)
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(out), _bits(want)), f"replay {r} differs"
