@@ -596,6 +596,8 @@ def measure_attention(workload: str, batch, out, steps: int, warmup: int, worker
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic,
             "traffic_over_algorithmic": None if traffic is None else round(traffic / nbytes, 4),
+            # the HBM bytes the counters saw per launch over this run's kernel time
+            "traffic_GBps": None if traffic is None else round(traffic / (kern_avg * 1e-3) / 1e9, 2),
             "kernel_ms": round(kern_avg, 5),
             "ms_per_step_with_kernel_events": round(t_b0.elapsed_time(t_b1) / steps, 5),
             "kernel_ms_p10_p90": [round(float(np.percentile(kern_ms, 10)), 5),
