@@ -4,6 +4,7 @@ Every call compiles from scratch; the library lands next to this file.
 """
 from __future__ import annotations
 
+import glob
 import os
 import subprocess
 import sys
@@ -78,7 +79,6 @@ def clang_runtime(name: str) -> str | None:
     """A sanitizer runtime of the compiler hipcc drives (``asan`` or ``ubsan_standalone``), to
     preload into an uninstrumented Python."""
     rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
-    import glob
     hits = sorted(glob.glob(os.path.join(rocm, "llvm", "lib", "clang", "*", "lib", "linux",
                                          f"libclang_rt.{name}-x86_64.so")))
     return hits[-1] if hits else None
