@@ -22,9 +22,9 @@
  * page; a finished sample's pages return to the stack last block first.
  *
  * Every step, on desc.stream and in this order: new prompt pages are filled;
- * the step's new K/V rows are stored (the caller's k_new / v_new buffers, the
- * same every step, with the quantise-on-write of sl_kv_append_fp8 for an
- * E4M3 cache) and the step's sequence lengths and new block-table entries are
+ * the step's new K/V rows are stored (a set of the caller's k_new / v_new
+ * rows: one set every step, or the sets in turn with row_sets > 1; with the
+ * quantise-on-write of sl_kv_append_fp8 for an E4M3 cache) and the step's sequence lengths and new block-table entries are
  * written into seq_lens and block_table, all read by the device from a mapped
  * pinned staging buffer; the step's attention output (sl_decode_attn or
  * _fp8) is computed into `out` with the caller's q. Slots without a sample
@@ -89,7 +89,7 @@ typedef struct sl_engine_buffers {
        num_pages, num_workers, stream and workspace as for sl_decode_attn. */
     sl_attn_desc desc;
     const uint16_t *q;          /* bf16 [BS][Hq][D], used every step */
-    const uint16_t *k_new;      /* bf16 [BS][Hkv][D], appended every step */
+    const uint16_t *k_new;      /* bf16 [R][BS][Hkv][D], R = max(1, row_sets): step s appends set s % R */
     const uint16_t *v_new;
     void *k_pages;              /* bf16 or E4M3 [num_pages][Hkv][16][D] */
     void *v_pages;
@@ -101,6 +101,8 @@ typedef struct sl_engine_buffers {
     uint16_t *out_history;      /* optional (NULL): bf16 [history_steps][BS][Hq][D]; step s's output is
                                    copied to entry s (s < history_steps), one device copy per step */
     int32_t history_steps;      /* >= 0; entries of out_history */
+    int32_t row_sets;           /* >= 0; sets of new rows in k_new / v_new (0 and 1: one set, appended
+                                   every step) */
 } sl_engine_buffers;
 
 /*

@@ -63,7 +63,7 @@ bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 struct sl_engine {
     sl_engine_buffers buf{};
     sl_attn_desc step_desc{};          // buf.desc without timing events
-    int M = 0, BS = 0, max_blocks = 0, num_pages = 0, Hkv = 0, D = 0;
+    int M = 0, BS = 0, max_blocks = 0, num_pages = 0, Hkv = 0, D = 0, row_sets = 1;
     bool fp8 = false;
     uint32_t seed = 0;
     float attn_scale = 0.f;
@@ -107,7 +107,7 @@ struct sl_engine {
 
     // A step's staging: ring slot, update and fill counts, active samples.
     struct Staged {
-        int ring = 0, n_upd = 0, n_fill = 0, n_active = 0;
+        int ring = 0, n_upd = 0, n_fill = 0, n_active = 0, step = 0;
     };
     // The next step's staging: not prepared yet, prepared but not launched
     // (it admits prompts), or applied and appended by the last merge launch.
@@ -178,6 +178,7 @@ sl_status sl_engine::prepare(Staged &out)
         h[BS + b] = pages[b][t / kPageSize];
     }
     out.ring = r;
+    out.step = step;   // the step these rows belong to (prepare runs after the previous step's ++step)
     out.n_upd = (int)upd.size() / 3;
     out.n_fill = (int)fills.size();
     if (!upd.empty())   // (an empty vector's data() may be null, which memcpy must not get)
@@ -190,8 +191,9 @@ sl_status sl_engine::prepare(Staged &out)
 sl::AppendParams sl_engine::append_params(const Staged &sg) const
 {
     sl::AppendParams ap;
-    ap.k_new = buf.k_new;
-    ap.v_new = buf.v_new;
+    const size_t set = (size_t)(sg.step % row_sets) * BS * Hkv * D;   // this step's set of new rows
+    ap.k_new = buf.k_new + set;
+    ap.v_new = buf.v_new + set;
     ap.block_table = nullptr;   // the lengths and token pages come from the staging buffer
     ap.seq_lens = nullptr;
     ap.k_pages = buf.k_pages;
@@ -420,7 +422,7 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
         return SL_ERR_WORKSPACE;
     const int M = cfg->num_samples, BS = d.batch;
     if (M < 1 || BS < 1 || (cfg->admission != 0 && cfg->admission != 1) ||
-        (cfg->launch_mode != 0 && cfg->launch_mode != 1) || bufs->history_steps < 0)
+        (cfg->launch_mode != 0 && cfg->launch_mode != 1) || bufs->history_steps < 0 || bufs->row_sets < 0)
         return SL_ERR_SHAPE;
     if (bufs->history_steps > 0 && !bufs->out_history)
         return SL_ERR_NULL;
@@ -461,6 +463,7 @@ sl_status sl_engine_create(const sl_engine_config *cfg, const sl_engine_buffers 
     e->Hkv = d.num_kv_heads;
     e->D = d.head_dim;
     e->fp8 = fp8;
+    e->row_sets = std::max(1, (int)bufs->row_sets);
     e->seed = cfg->fill_seed;
     e->attn_scale = cfg->attn_scale;
     e->prompt.assign(cfg->prompt_len, cfg->prompt_len + M);

@@ -44,6 +44,7 @@ class Buffers(ctypes.Structure):
         ("out", ctypes.c_void_p),
         ("out_history", ctypes.c_void_p),
         ("history_steps", ctypes.c_int32),
+        ("row_sets", ctypes.c_int32),
     ]
 
 
@@ -66,15 +67,18 @@ class Engine:
 
     Allocates (with torch) the page pool, block table, lengths, query and
     new-row buffers, output and workspace; ``q``/``k_new``/``v_new`` hold
-    seeded random rows used in every step. ``two_launch`` makes every step
-    run the split kernel and the merge; ``history_steps`` > 0 keeps the
-    outputs of the first that many steps in ``history``.
+    seeded random rows used in every step (with ``row_sets`` > 1, ``k_new`` and
+    ``v_new`` hold that many sets [R][BS][Hkv][D] and step s appends set
+    s % R). ``two_launch`` makes every step run the split kernel and the
+    merge; ``history_steps`` > 0 keeps the outputs of the first that many
+    steps in ``history``.
     """
 
     def __init__(self, prompt_len, output_len, est_len=None, *, batch_slots: int, num_q_heads: int,
                  num_kv_heads: int, head_dim: int, kv_fp8: bool = False, lpt: bool = True,
                  num_pages: int | None = None, max_blocks: int | None = None, seed: int = 0,
-                 num_workers: int = 0, two_launch: bool = False, history_steps: int = 0, device="cuda:0"):
+                 num_workers: int = 0, two_launch: bool = False, history_steps: int = 0, row_sets: int = 1,
+                 device="cuda:0"):
         self.prompt_len = np.ascontiguousarray(prompt_len, dtype=np.int32)
         self.output_len = np.ascontiguousarray(output_len, dtype=np.int32)
         self.est_len = np.ascontiguousarray(self.output_len if est_len is None else est_len, dtype=np.int32)
@@ -95,8 +99,9 @@ class Engine:
         self.block_table = torch.zeros((batch_slots, self.max_blocks), dtype=torch.int32, device=dev)
         self.seq_lens = torch.zeros(batch_slots, dtype=torch.int32, device=dev)
         self.q = torch.randn((batch_slots, num_q_heads, head_dim), generator=g, device=dev).to(torch.bfloat16)
-        self.k_new = torch.randn((batch_slots, num_kv_heads, head_dim), generator=g, device=dev).to(torch.bfloat16)
-        self.v_new = torch.randn((batch_slots, num_kv_heads, head_dim), generator=g, device=dev).to(torch.bfloat16)
+        rows = ((row_sets,) if row_sets > 1 else ()) + (batch_slots, num_kv_heads, head_dim)
+        self.k_new = torch.randn(rows, generator=g, device=dev).to(torch.bfloat16)
+        self.v_new = torch.randn(rows, generator=g, device=dev).to(torch.bfloat16)
         self.out = torch.zeros((batch_slots, num_q_heads, head_dim), dtype=torch.bfloat16, device=dev)
         self.history = (torch.zeros((history_steps, batch_slots, num_q_heads, head_dim), dtype=torch.bfloat16,
                                     device=dev) if history_steps > 0 else None)
@@ -110,7 +115,8 @@ class Engine:
         ptr = lambda t: None if t is None else t.data_ptr()
         self._bufs = Buffers(desc, ptr(self.q), ptr(self.k_new), ptr(self.v_new), ptr(self.k_pages),
                              ptr(self.v_pages), ptr(self.k_scales), ptr(self.v_scales), ptr(self.block_table),
-                             ptr(self.seq_lens), ptr(self.out), ptr(self.history), int(history_steps))
+                             ptr(self.seq_lens), ptr(self.out), ptr(self.history), int(history_steps),
+                             int(row_sets))
         self._cfg = Config(M, 1 if lpt else 0, 1 if kv_fp8 else 0, seed & 0xFFFFFFFF, self.scale,
                            self.prompt_len.ctypes.data, self.output_len.ctypes.data, self.est_len.ctypes.data,
                            1 if two_launch else 0)

@@ -181,6 +181,8 @@ def test_engine_rejects_bad_arguments(lib):
     for hist, steps, status in [(None, 3, -1), (FAKE, -1, -2), (FAKE + 8, 1, -6)]:
         b = E.Buffers(d, *([FAKE] * 10), hist, steps)
         assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(b), ctypes.byref(handle)) == status
+    b = E.Buffers(d, *([FAKE] * 10), None, 0, -1)   # a negative number of row sets
+    assert lib.sl_engine_create(ctypes.byref(cfg), ctypes.byref(b), ctypes.byref(handle)) == -2
     n = ctypes.c_int32(0)
     assert lib.sl_engine_run(None, 1, ctypes.byref(n)) == -1
     assert lib.sl_engine_destroy(None) == 0

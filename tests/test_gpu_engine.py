@@ -261,3 +261,70 @@ def test_engine_launch_modes_agree_on_random_shapes(kv, case):
     err = (h1 - h2).abs()
     assert torch.isfinite(h1).all() and torch.isfinite(h2).all()
     assert not (err > ulp + 1e-5).any(), f"max |diff| {float(err.max()):.3g}"
+
+
+@pytest.mark.parametrize("kv", ["e4m3", "bf16"])
+def test_engine_rows_that_change_every_step(kv):
+    """Row sets of growing magnitude (x1, x4, x16, x64, x256, in turn): with an E4M3 cache every
+    append after a smaller set raises its page's scale and re-encodes rows that the same step's
+    attention reads (any page holding generated rows of two sets has been re-encoded). The
+    one-launch step appends a unit's row only after the unit's reads, so both launch modes must
+    leave the same codes and scales, bit for bit, and the same per-step outputs (zero queries: to
+    the last bf16 place); the last step also matches the oracle on the device cache. With a bf16
+    cache every generated token of the samples that finish in the last step holds its step's set."""
+    rng = np.random.default_rng(91)
+    M, BS, Hq, Hkv, D, R = 20, 6, 8, 2, 128, 5
+    prompt = rng.choice(np.array([0, 3, 16, 21, 40, 77], np.int32), M)
+    out = np.clip(np.exp(rng.normal(np.log(30), 0.8, M)), 2, 100).astype(np.int32)
+    need = int(((prompt + out + 15) // 16).max())
+    ref = S.simulate(prompt, out, out, BS, BS * need, need, "lpt")
+    steps = ref.makespan
+    assert int(out.max()) >= 17   # some page holds generated rows of several sets
+    fp8 = kv == "e4m3"
+    hist, cache = {}, {}
+    for two in (False, True):
+        eng = E.Engine(prompt, out, out, batch_slots=BS, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, lpt=True,
+                       kv_fp8=fp8, seed=5, two_launch=two, history_steps=steps, row_sets=R)
+        scale = (4.0 ** torch.arange(R, device=DEV, dtype=torch.float32)).view(R, 1, 1, 1)
+        eng.k_new.copy_((eng.k_new.float() * scale).to(torch.bfloat16))
+        eng.v_new.copy_((eng.v_new.float() * scale).to(torch.bfloat16))
+        eng.q.zero_()
+        assert eng.run() == steps
+        torch.cuda.synchronize()
+        hist[two] = eng.history.float().cpu()
+        kp = eng.k_pages.cpu().numpy() if fp8 else _host_u16(eng.k_pages)
+        vp = eng.v_pages.cpu().numpy() if fp8 else _host_u16(eng.v_pages)
+        ks = eng.k_scales.cpu().numpy() if fp8 else None
+        vs = eng.v_scales.cpu().numpy() if fp8 else None
+        lens, table = eng.seq_lens.cpu().numpy(), eng.block_table.cpu().numpy()
+        cache[two] = (kp, vp, ks, vs, lens, table)
+        if not fp8 and not two:   # token t of sample i, made in step admit + (t - p), holds that step's set
+            kn = _host_u16(eng.k_new)
+            for i in range(M):
+                b = ref.slot[i]
+                if ref.finish_step[i] != steps - 1:
+                    continue   # finished earlier: its pages may have been handed out again
+                for t in range(int(prompt[i]), int(prompt[i] + out[i])):
+                    step = ref.admit_step[i] + (t - int(prompt[i]))
+                    assert np.array_equal(kp[table[b, t // 16], :, t % 16, :], kn[step % R, b]), (i, t)
+        if not two:
+            kw = dict(k_scales=ks, v_scales=vs) if fp8 else {}
+            want = oracle.decode_attn(_host_u16(eng.q), kp, vp, table, lens, eng.scale, **kw)
+            if fp8:
+                vdq = torch.from_numpy(vp).view(torch.float8_e4m3fn).double().numpy() * vs[:, :, None, None]
+            else:
+                vdq = torch.from_numpy(vp.view(np.int16)).view(torch.bfloat16).double().numpy()
+            parity.assert_parity(eng.out, want, "last step",
+                                 value_scale=parity.value_rms_rows(vdq, table, lens, Hq))
+        eng.close()
+    for x, y, name in zip(cache[False], cache[True], ("k pages", "v pages", "k scales", "v scales", "lengths",
+                                                      "block table")):
+        if x is not None:
+            assert np.array_equal(x.view(np.uint8) if x.dtype != np.int32 else x,
+                                  y.view(np.uint8) if y.dtype != np.int32 else y), f"{name} differ"
+    a, b = hist[False], hist[True]
+    assert torch.isfinite(a).all() and torch.isfinite(b).all()
+    mag = torch.maximum(a.abs(), b.abs()).clamp_min(2.0 ** -126)
+    ulp = torch.exp2(torch.floor(torch.log2(mag)) - 7)
+    err = (a - b).abs()
+    assert not (err > ulp + 1e-5 * mag.clamp_min(1.0)).any(), f"max |diff| {float(err.max()):.3g}"
